@@ -1,0 +1,373 @@
+"""Plain fp64 CPU oracle of SPADE's block-sparse attention hot path.
+
+TEST INFRASTRUCTURE ONLY. This module is the slow, obviously-correct reference
+that the GPU path is checked against. Only the test suite, the smoke check and
+the benchmark's CPU-baseline leg may import it; the library never does, and it
+shares no code with the GPU kernels.
+
+Paper: "SPADE: An Input-Adaptive Sparse Attention Engine for Fast Video
+Diffusion Models Inference" (arXiv 2608.03335). What the path computes, in the
+paper's order (§3.3, Head-wise Sparse Attention):
+
+  1. blocking: rearrange tokens into 3D blocks of a blocking scheme
+     (§3.1, Fig. 3: t x h x w tiles, order T, H, W);
+  2. Summarizer: one vector per Q/K block, here the mean (MEAN-SPADE, §3.1);
+  3. inter-block Estimator: block-pair importance from the summaries' dot
+     products (§3.3);
+  4. Top-K / Top-P filtering of each query block's row (§3.1 utility
+     parameters, §3.3);
+  5. block-sparse attention, Eq. (2): softmax(QK^T/sqrt(d) + M) V with M = 0
+     on kept block pairs and -inf elsewhere;
+  6. restore the original token layout (§3.3).
+Plus the intra-block aggregation measure SICS, Eq. (4) and Eq. (5) / Alg. 1
+(§3.2), and the Aggregation Score, Eq. (3).
+
+Readings where the paper is silent (each is a stated choice, listed with the
+design notes):
+  * tokens are flattened T-major, n = (t*Hs + y)*Ws + x;
+  * blocks are numbered T-major over the ceil-sized block grid; inside a block
+    the valid tokens come first, in raster order of (dt, dy, dx); the remaining
+    slots up to BS are zero padding;
+  * block means average valid tokens only; padded keys never receive weight;
+  * the estimator score is <qbar_i, kbar_j> / sqrt(d);
+  * rows are ranked by (score descending, block index ascending);
+  * Top-P keeps the shortest prefix of that ranking whose softmax mass over the
+    row's block scores reaches tau (at least one block); tau >= 1 keeps all;
+  * kept indices are reported in ascending block order.
+
+Every array here is float64 (inputs are upcast first). Shapes: Q, K, V are
+[B, H, N, d]; blocked tensors are [B, H, NB*BS, d].
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# Geometry (§3.1 blocking scheme, Fig. 3; §2.1 flattening of the latent grid)
+# --------------------------------------------------------------------------
+@dataclass(frozen=True)
+class Geometry:
+    T: int
+    Hs: int
+    Ws: int
+    bt: int
+    bh: int
+    bw: int
+
+    @property
+    def N(self) -> int:
+        return self.T * self.Hs * self.Ws
+
+    @property
+    def BS(self) -> int:
+        return self.bt * self.bh * self.bw
+
+    @property
+    def grid(self):
+        return (-(-self.T // self.bt), -(-self.Hs // self.bh), -(-self.Ws // self.bw))
+
+    @property
+    def NB(self) -> int:
+        nT, nH, nW = self.grid
+        return nT * nH * nW
+
+
+def block_tables(g: Geometry):
+    """Enumerate every block and its valid tokens.
+
+    Returns (slot_token, n_valid):
+      slot_token[p] for p in [0, NB*BS): the raster token index stored at padded
+        position p, or -1 for a padding slot;
+      n_valid[b]: number of real tokens in block b.
+    Blocks are visited in T-major order of the block grid; within a block the
+    tokens are visited in raster order of (dt, dy, dx) and placed in consecutive
+    slots, so real tokens come first.
+    """
+    nT, nH, nW = g.grid
+    BS = g.BS
+    slot_token = np.full(g.NB * BS, -1, dtype=np.int64)
+    n_valid = np.zeros(g.NB, dtype=np.int64)
+    b = 0
+    for tb in range(nT):
+        for hb in range(nH):
+            for wb in range(nW):
+                s = 0
+                for dt in range(g.bt):
+                    for dy in range(g.bh):
+                        for dx in range(g.bw):
+                            t, y, x = tb * g.bt + dt, hb * g.bh + dy, wb * g.bw + dx
+                            if t < g.T and y < g.Hs and x < g.Ws:
+                                slot_token[b * BS + s] = (t * g.Hs + y) * g.Ws + x
+                                s += 1
+                n_valid[b] = s
+                b += 1
+    return slot_token, n_valid
+
+
+def token_position(g: Geometry) -> np.ndarray:
+    """pos[n] = padded position of raster token n (inverse of slot_token)."""
+    slot_token, _ = block_tables(g)
+    pos = np.empty(g.N, dtype=np.int64)
+    valid = slot_token >= 0
+    pos[slot_token[valid]] = np.nonzero(valid)[0]
+    return pos
+
+
+# --------------------------------------------------------------------------
+# Blocking (layout transform) and its inverse (§3.3: "rearranged into a
+# blocked layout"; "output blocks are restored to the original layout")
+# --------------------------------------------------------------------------
+def reorder(X: np.ndarray, g: Geometry) -> np.ndarray:
+    """Raster [.., N, d] -> blocked [.., NB*BS, d]; padding slots are zero."""
+    slot_token, _ = block_tables(g)
+    out = np.zeros(X.shape[:-2] + (g.NB * g.BS, X.shape[-1]), dtype=X.dtype)
+    valid = slot_token >= 0
+    out[..., valid, :] = X[..., slot_token[valid], :]
+    return out
+
+
+def inverse_reorder(Xb: np.ndarray, g: Geometry) -> np.ndarray:
+    """Blocked [.., NB*BS, d] -> raster [.., N, d] (padding slots dropped)."""
+    return Xb[..., token_position(g), :]
+
+
+# --------------------------------------------------------------------------
+# Summarizer: mean over each block's valid tokens (§3.1, MEAN-SPADE)
+# --------------------------------------------------------------------------
+def block_means(Xb: np.ndarray, g: Geometry) -> np.ndarray:
+    """[B, H, NB*BS, d] -> [B, H, NB, d], mean over valid slots only."""
+    _, n_valid = block_tables(g)
+    Xb = np.asarray(Xb, dtype=np.float64)
+    out = np.empty(Xb.shape[:-2] + (g.NB, Xb.shape[-1]), dtype=np.float64)
+    for b in range(g.NB):
+        rows = Xb[..., b * g.BS: b * g.BS + n_valid[b], :]
+        out[..., b, :] = rows.sum(axis=-2) / n_valid[b]
+    return out
+
+
+# --------------------------------------------------------------------------
+# SICS (§3.2): sum of all pairwise cosine similarities inside one block.
+# Three forms that must agree: Eq. (4) directly; Alg. 1 (online partial sums,
+# from the last line of Eq. (5)); and the squared norm of the sum of unit
+# vectors, which Eq. (5)'s expansion equals term by term.
+# --------------------------------------------------------------------------
+def _unit_rows(Q: np.ndarray) -> np.ndarray:
+    Q = np.asarray(Q, dtype=np.float64)
+    nrm = np.sqrt((Q * Q).sum(axis=-1, keepdims=True))
+    safe = np.where(nrm > 0, nrm, 1.0)
+    return np.where(nrm > 0, Q / safe, 0.0)  # a zero vector contributes nothing
+
+
+def sics_pairwise(Q: np.ndarray) -> float:
+    """Eq. (4): sum_a sum_b q_a.q_b / (|q_a| |q_b|) for one block [n, d]."""
+    U = _unit_rows(Q)
+    n = U.shape[0]
+    total = 0.0
+    for a in range(n):
+        for b in range(n):
+            total += float(U[a] @ U[b])
+    return total
+
+
+def sics_online(Q: np.ndarray) -> float:
+    """Alg. 1: running sum r of unit vectors; sigma += <r, q_j>; return 2 sigma + n.
+
+    The "+ n" counts the diagonal; a zero row has no unit vector, so it adds
+    neither to sigma nor to the diagonal count.
+    """
+    U = _unit_rows(Q)
+    r = np.zeros(U.shape[1])
+    sigma = 0.0
+    diag = 0
+    for j in range(U.shape[0]):
+        sigma += float(r @ U[j])
+        r = r + U[j]
+        diag += int(np.any(U[j] != 0))
+    return 2.0 * sigma + diag
+
+
+def sics_closed(Q: np.ndarray) -> float:
+    """|| sum_k q_k/|q_k| ||^2, the O(n d) form of Eq. (4)."""
+    s = _unit_rows(Q).sum(axis=0)
+    return float(s @ s)
+
+
+def block_sics(Xb: np.ndarray, g: Geometry, form: str = "closed") -> np.ndarray:
+    """[B, H, NB*BS, d] -> [B, H, NB] SICS of each block's valid rows."""
+    fn = {"closed": sics_closed, "online": sics_online, "pairwise": sics_pairwise}[form]
+    _, n_valid = block_tables(g)
+    lead = Xb.shape[:-2]
+    out = np.empty(lead + (g.NB,), dtype=np.float64)
+    for idx in np.ndindex(*lead):
+        for b in range(g.NB):
+            out[idx + (b,)] = fn(Xb[idx + (slice(b * g.BS, b * g.BS + n_valid[b]),)])
+    return out
+
+
+def aggregation_score(sics: np.ndarray, g: Geometry):
+    """Eq. (3): AS = sum over blocks of SICS (last axis), raw and normalised.
+
+    The normalised form divides by sum_b n_b^2 (the value when every block's
+    vectors are parallel) so that candidates with different block sizes or
+    padding are comparable; for equal, unpadded blocks it is a constant factor
+    and leaves the per-head argmax of Eq. (3) unchanged.
+    """
+    _, n_valid = block_tables(g)
+    raw = sics.sum(axis=-1)
+    return raw, raw / float((n_valid.astype(np.float64) ** 2).sum())
+
+
+# --------------------------------------------------------------------------
+# Inter-block estimator (§3.3): importance of block pair (i, j) from summaries
+# --------------------------------------------------------------------------
+def block_scores(qbar: np.ndarray, kbar: np.ndarray, scale: float) -> np.ndarray:
+    """[.., NB, d] x [.., NB, d] -> [.., NB, NB]: <qbar_i, kbar_j> * scale."""
+    return np.matmul(qbar, np.swapaxes(kbar, -1, -2)) * scale
+
+
+# --------------------------------------------------------------------------
+# Top-K / Top-P index search (§3.1 utility parameters; §3.3 filtering)
+# --------------------------------------------------------------------------
+def rank_order(s: np.ndarray) -> np.ndarray:
+    """Block indices of one row ordered by (score descending, index ascending)."""
+    j = np.arange(s.shape[0])
+    return np.lexsort((j, -s))
+
+
+def row_softmax(s: np.ndarray) -> np.ndarray:
+    e = np.exp(s - s.max())
+    return e / e.sum()
+
+
+def select_row_topk(s: np.ndarray, k: int) -> np.ndarray:
+    """Ascending indices of the min(k, NB) highest-ranked blocks."""
+    return np.sort(rank_order(s)[: min(k, s.shape[0])])
+
+
+def select_row_topp(s: np.ndarray, tau: float) -> np.ndarray:
+    """Ascending indices of the shortest ranked prefix whose mass reaches tau.
+
+    The mass of block j is its softmax weight over the row's scores; the prefix
+    mass is accumulated left to right in rank order. At least one block is
+    kept. With tau >= 1 every block is kept (exact softmax weights are all
+    positive, so no proper prefix reaches 1). If rounding keeps the running sum
+    below tau to the end, every block is kept.
+    """
+    NB = s.shape[0]
+    if tau >= 1.0:
+        return np.arange(NB)
+    order = rank_order(s)
+    cum = np.cumsum(row_softmax(s)[order])  # sequential, left to right
+    hit = np.nonzero(cum >= tau)[0]
+    m = int(hit[0]) + 1 if hit.size else NB
+    return np.sort(order[:m])
+
+
+def select(scores: np.ndarray, mode: str, topk: int | None = None, tau: float | None = None):
+    """Apply the row rule to every (b, h, i) row of [B, H, NB, NB] scores.
+
+    Returns counts [B, H, NB] int32 and indices [B, H, NB, NB] int32 whose
+    first counts[..] entries are the kept blocks, ascending; the rest are -1.
+    """
+    lead = scores.shape[:-1]
+    NB = scores.shape[-1]
+    counts = np.zeros(lead, dtype=np.int32)
+    indices = np.full(lead + (NB,), -1, dtype=np.int32)
+    for idx in np.ndindex(*lead):
+        row = scores[idx]
+        kept = select_row_topk(row, topk) if mode == "topk" else select_row_topp(row, tau)
+        counts[idx] = kept.size
+        indices[idx + (slice(0, kept.size),)] = kept
+    return counts, indices
+
+
+def block_mask(counts: np.ndarray, indices: np.ndarray) -> np.ndarray:
+    """Binary [.., NB, NB] mask from counts + index lists."""
+    NB = indices.shape[-1]
+    mask = np.zeros(indices.shape[:-1] + (NB,), dtype=bool)
+    for idx in np.ndindex(*counts.shape):
+        mask[idx + (indices[idx][: counts[idx]],)] = True
+    return mask
+
+
+# --------------------------------------------------------------------------
+# Attention: Eq. (1) dense and Eq. (2) block-sparse
+# --------------------------------------------------------------------------
+def dense_attention(Q, K, V, scale: float):
+    """Eq. (1) on [.., N, d]: softmax(Q K^T * scale) V, max-subtracted, fp64."""
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    logits = np.matmul(Q, np.swapaxes(K, -1, -2)) * scale
+    logits -= logits.max(axis=-1, keepdims=True)
+    w = np.exp(logits)
+    w /= w.sum(axis=-1, keepdims=True)
+    return np.matmul(w, V)
+
+
+def block_sparse_attention(Qb, Kb, Vb, counts, indices, g: Geometry, scale: float,
+                           rows=None):
+    """Eq. (2) on blocked tensors, one query block at a time.
+
+    For query block i of head (b, h), the keys are the valid slots of the kept
+    blocks S_i (ascending). Returns (Ob, lse): Ob [B, H, NB*BS, d] with padding
+    query slots left at 0, lse [B, H, NB*BS] (natural log of the softmax
+    denominator, including the max), 0 at padding slots.
+
+    rows: optional iterable of (b, h, i) to compute only those query blocks
+    (the others stay 0); used for sampled checks at full size.
+    """
+    _, n_valid = block_tables(g)
+    BS = g.BS
+    B, H = Qb.shape[:2]
+    d = Qb.shape[-1]
+    Ob = np.zeros((B, H, g.NB * BS, d), dtype=np.float64)
+    lse = np.zeros((B, H, g.NB * BS), dtype=np.float64)
+    todo = rows if rows is not None else np.ndindex(B, H, g.NB)
+    for (b, h, i) in todo:
+        kept = indices[b, h, i, : counts[b, h, i]]
+        q = np.asarray(Qb[b, h, i * BS: i * BS + n_valid[i]], dtype=np.float64)
+        ks = np.concatenate([np.asarray(Kb[b, h, j * BS: j * BS + n_valid[j]], dtype=np.float64)
+                             for j in kept])
+        vs = np.concatenate([np.asarray(Vb[b, h, j * BS: j * BS + n_valid[j]], dtype=np.float64)
+                             for j in kept])
+        logits = (q @ ks.T) * scale
+        mx = logits.max(axis=1, keepdims=True)
+        w = np.exp(logits - mx)
+        z = w.sum(axis=1, keepdims=True)
+        Ob[b, h, i * BS: i * BS + n_valid[i]] = (w @ vs) / z
+        lse[b, h, i * BS: i * BS + n_valid[i]] = (mx + np.log(z))[:, 0]
+    return Ob, lse
+
+
+# --------------------------------------------------------------------------
+# Whole path and work counters
+# --------------------------------------------------------------------------
+def spade_attention(Q, K, V, g: Geometry, mode: str, topk=None, tau=None, scale=None):
+    """blocking -> means -> scores -> selection -> Eq. (2) -> restore layout."""
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    d = Q.shape[-1]
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    Qb, Kb, Vb = reorder(Q, g), reorder(K, g), reorder(V, g)
+    qbar, kbar = block_means(Qb, g), block_means(Kb, g)
+    s = block_scores(qbar, kbar, scale)
+    counts, indices = select(s, mode, topk=topk, tau=tau)
+    Ob, lse = block_sparse_attention(Qb, Kb, Vb, counts, indices, g, scale)
+    return dict(O=inverse_reorder(Ob, g), Ob=Ob, lse=lse, qbar=qbar, kbar=kbar,
+                scores=s, counts=counts, indices=indices)
+
+
+def kept_flops(counts, indices, g: Geometry, d: int) -> float:
+    """Matmul FLOPs of the kept work: sum over kept (i, j) of 4 * n_i * n_j * d."""
+    _, n_valid = block_tables(g)
+    total = 0
+    for idx in np.ndindex(*counts.shape):
+        i = idx[-1]
+        kept = indices[idx][: counts[idx]]
+        total += 4 * int(n_valid[i]) * int(n_valid[kept].sum()) * d
+    return float(total)
+
+
+def block_sparsity(counts, NB: int) -> float:
+    return 1.0 - float(np.asarray(counts, dtype=np.float64).sum()) / (counts.size * NB)
