@@ -1,0 +1,156 @@
+/*
+ * spade.h — C ABI of the MI355X (gfx950) block-sparse attention hot path of
+ * SPADE (arXiv 2608.03335, "An Input-Adaptive Sparse Attention Engine for Fast
+ * Video Diffusion Models Inference").
+ *
+ * The path (paper §3.3, Head-wise Sparse Attention), one call per step:
+ *   spade_block_reorder      blocking / layout transform and its inverse
+ *   spade_summarize          Summarizer (block means) + optional SICS (§3.2)
+ *   spade_estimate_select    inter-block Estimator + Top-K / Top-P index search
+ *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
+ *
+ * Conventions shared by every call
+ *   - All tensor pointers are DEVICE pointers, owned by the caller, contiguous,
+ *     16-byte aligned. The library never allocates, frees or synchronises, and
+ *     keeps no state; calls are reentrant and asynchronous on `stream`.
+ *   - Shapes follow the paper's problem statement: B batches, H heads, N tokens
+ *     of head dimension d, where the N tokens form a (T, Hs, Ws) latent grid
+ *     flattened T-major: token n = (t*Hs + y)*Ws + x (§2.1).
+ *   - A blocking scheme (bt, bh, bw) tiles the grid (§3.1, Fig. 3). The block
+ *     grid is ceil(T/bt) x ceil(Hs/bh) x ceil(Ws/bw), NB blocks numbered
+ *     T-major; BS = bt*bh*bw slots per block. Inside a block the n_b real tokens
+ *     occupy slots 0..n_b-1 in raster order of (dt, dy, dx); slots n_b..BS-1 are
+ *     padding (only blocks at the grid's far edges have them).
+ *   - "Blocked" tensors are [B, H, NB*BS, d]; raster tensors [B, H, N, d].
+ *   - Errors: argument checks run on the host before any launch and return a
+ *     status (no partial work). A launch failure returns SPADE_ERR_HIP. Device
+ *     faults surface at the caller's next synchronisation. spade_last_error()
+ *     gives a message for the calling thread's most recent failure.
+ *   - Limits: d in {64, 128}; BS <= 256; NB <= 1024 for the selection call.
+ *     B, H, T, Hs or Ws equal to 0 is an empty problem: the call returns
+ *     SPADE_OK without launching anything (pointers are then not read).
+ */
+#ifndef SPADE_H
+#define SPADE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPADE_OK = 0,
+  SPADE_ERR_INVALID_ARG = 1, /* null pointer, bad shape, bad mode/parameter  */
+  SPADE_ERR_UNSUPPORTED = 2, /* valid but outside the limits above           */
+  SPADE_ERR_WORKSPACE = 3,   /* workspace missing or too small               */
+  SPADE_ERR_HIP = 4          /* a HIP launch or query failed                 */
+} spade_status;
+
+enum { SPADE_BF16 = 0, SPADE_FP32 = 1 };  /* element type of spade_block_reorder */
+enum { SPADE_TOPK = 0, SPADE_TOPP = 1 };  /* row rule of spade_estimate_select   */
+
+/* Problem geometry: batch, heads, head dim; latent grid; blocking scheme. */
+typedef struct {
+  int32_t B, H, d;
+  int32_t T, Hs, Ws;
+  int32_t bt, bh, bw;
+} spade_geom;
+
+/*
+ * Blocking (layout transform) and its inverse — paper §3.3: Q, K, V are
+ * rearranged into the blocked layout of the selected scheme for intra-block
+ * contiguity, and output blocks are restored to the original layout.
+ *
+ *   inverse == 0: x is raster [B,H,N,d], y is blocked [B,H,NB*BS,d];
+ *                 y[.., b*BS+s, :] = x[.., token(b,s), :] for real slots,
+ *                 0 for padding slots (every element of y is written).
+ *   inverse == 1: x is blocked, y is raster; padding slots of x are not read.
+ *   dtype: SPADE_BF16 (2-byte elements) or SPADE_FP32 (4-byte). Bit-exact copy.
+ *   x and y must not overlap.
+ */
+spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y,
+                                 int32_t dtype, int32_t inverse, hipStream_t stream);
+
+/*
+ * Summarizer and intra-block estimator — paper §3.1 (Summarizer = mean,
+ * MEAN-SPADE) and §3.2, Eq. (4)/(5), Alg. 1 (SICS).
+ *
+ *   qb, kb:       blocked bf16 [B,H,NB*BS,d] (output of spade_block_reorder).
+ *   qbar, kbar:   out, fp64 [B,H,NB,d]: mean over each block's real tokens
+ *                 (accumulated in fp64).
+ *   sics_q, sics_k: out, nullable, fp64 [B,H,NB]: SICS of each block's real
+ *                 rows, computed as |sum_k q_k/|q_k||^2 (equal to Eq. (4); a
+ *                 zero row contributes nothing). Pass both or neither.
+ */
+spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb,
+                             double* qbar, double* kbar, double* sics_q, double* sics_k,
+                             hipStream_t stream);
+
+/*
+ * Inter-block Estimator + Top-K / Top-P index search — paper §3.3 (inter-block
+ * importance matrix of size NB x NB from the Q/K summaries, filtered by Top-K
+ * or Top-P) with §3.1's Top-K/Top-P mode parameter.
+ *
+ *   score(i, j) = <qbar_i, kbar_j> * scale, in fp64 (scale is normally 1/sqrt(d)).
+ *   Each row (b, h, i) ranks blocks j by (score descending, j ascending) and keeps
+ *     SPADE_TOPK: the first min(topk, NB) blocks (topk >= 1; tau ignored);
+ *     SPADE_TOPP: the shortest prefix whose softmax mass over the row's scores
+ *                 reaches tau, at least one block; tau in (0, 1], tau == 1 keeps
+ *                 every block (topk ignored).
+ *   counts:  out, int32 [B,H,NB]: number of kept blocks per row.
+ *   indices: out, int32 [B,H,NB,NB]: row (b,h,i) holds its kept block indices in
+ *            ascending order in entries 0..counts-1; later entries are not written.
+ *   scores:  out, nullable, fp64 [B,H,NB,NB]: the score matrix (for checking).
+ *   Requires NB <= 1024.
+ */
+spade_status spade_estimate_select(const spade_geom* g, const double* qbar, const double* kbar,
+                                   int32_t mode, int32_t topk, double tau, double scale,
+                                   int32_t* counts, int32_t* indices, double* scores,
+                                   hipStream_t stream);
+
+/*
+ * Scratch bytes spade_block_sparse_attn needs for its work schedule (the
+ * ranked work list of §3.3's optimisation (3)); 0 for an empty problem.
+ */
+size_t spade_attn_workspace_bytes(const spade_geom* g);
+
+/*
+ * Flash block-sparse attention — paper Eq. (2) with block mask M (0 on kept
+ * block pairs, -inf elsewhere) and §3.3 optimisation (3): online softmax over the
+ * kept K/V blocks of each query block, never materialising the score matrix.
+ *
+ *   qb, kb, vb: blocked bf16 [B,H,NB*BS,d].
+ *   counts, indices: the block lists, in the layout spade_estimate_select writes.
+ *            Any lists are accepted; entries outside [0, NB) are skipped and
+ *            counts above NB are clamped, so malformed lists cannot fault.
+ *            Each kept block contributes its real key slots only.
+ *   scale:   logit scale (normally 1/sqrt(d)).
+ *   ob:      out, bf16 [B,H,NB*BS,d]: real query slots hold the attention output,
+ *            padding slots are written 0. A row with no kept block gets 0.
+ *   lse:     out, nullable, fp32 [B,H,NB*BS]: natural-log softmax denominator
+ *            (max included) per real query slot; padding slots are not written.
+ *   workspace: device scratch of at least spade_attn_workspace_bytes(g) bytes
+ *            (contents on entry do not matter).
+ *   bf16 MFMA with fp32 accumulation; softmax in fp32; P rounded to bf16 for
+ *   the P*V product; output rounded to bf16 (round to nearest even).
+ */
+spade_status spade_block_sparse_attn(const spade_geom* g, const void* qb, const void* kb,
+                                     const void* vb, const int32_t* counts,
+                                     const int32_t* indices, double scale, void* ob, float* lse,
+                                     void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char* spade_status_string(spade_status s);
+
+/* Message describing the calling thread's most recent non-OK status ("" if none). */
+const char* spade_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPADE_H */

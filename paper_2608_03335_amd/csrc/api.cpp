@@ -1,0 +1,181 @@
+// C-ABI entry points: host-side argument validation, then the kernel launchers.
+// Validation never touches the HIP runtime, so every error path runs without a GPU.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include "spade.h"
+#include "spade_internal.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+spade_status fail(spade_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks the geometry and fills `dg`. Sets *empty when there is nothing to do.
+spade_status check_geom(const spade_geom* g, spade::DevGeom* dg, bool* empty) {
+  if (!g) return fail(SPADE_ERR_INVALID_ARG, "geometry pointer is null");
+  if (g->B < 0 || g->H < 0 || g->T < 0 || g->Hs < 0 || g->Ws < 0)
+    return fail(SPADE_ERR_INVALID_ARG, "negative size (B=%d H=%d T=%d Hs=%d Ws=%d)", g->B, g->H,
+                g->T, g->Hs, g->Ws);
+  if (g->bt < 1 || g->bh < 1 || g->bw < 1)
+    return fail(SPADE_ERR_INVALID_ARG, "block dims must be >= 1 (got %d,%d,%d)", g->bt, g->bh,
+                g->bw);
+  if (g->d != 64 && g->d != 128)
+    return fail(SPADE_ERR_UNSUPPORTED, "head dim d=%d not supported (64 or 128)", g->d);
+  const int64_t BS = int64_t(g->bt) * g->bh * g->bw;
+  if (BS > spade::kMaxBS)
+    return fail(SPADE_ERR_UNSUPPORTED, "block size bt*bh*bw=%lld exceeds %d", (long long)BS,
+                spade::kMaxBS);
+  *empty = (g->B == 0 || g->H == 0 || g->T == 0 || g->Hs == 0 || g->Ws == 0);
+  dg->B = g->B; dg->H = g->H; dg->d = g->d;
+  dg->T = g->T; dg->Hs = g->Hs; dg->Ws = g->Ws;
+  dg->bt = g->bt; dg->bh = g->bh; dg->bw = g->bw;
+  dg->nT = (g->T + g->bt - 1) / g->bt;
+  dg->nH = (g->Hs + g->bh - 1) / g->bh;
+  dg->nW = (g->Ws + g->bw - 1) / g->bw;
+  const int64_t NB = int64_t(dg->nT) * dg->nH * dg->nW;
+  const int64_t N = int64_t(g->T) * g->Hs * g->Ws;
+  dg->N = N;
+  dg->BS = int(BS);
+  // Offsets are 64-bit in the kernels; keep per-head block counts and grid
+  // dimensions inside int32 and the largest tensor inside 2^40 elements.
+  if (NB > (int64_t(1) << 30) || N > (int64_t(1) << 31))
+    return fail(SPADE_ERR_UNSUPPORTED, "grid too large (N=%lld NB=%lld)", (long long)N,
+                (long long)NB);
+  const int64_t rows = int64_t(g->B) * g->H * NB * BS;
+  if (rows * g->d > (int64_t(1) << 40) || int64_t(g->B) * g->H > 65535)
+    return fail(SPADE_ERR_UNSUPPORTED, "tensor too large (B*H*NB*BS*d)");
+  dg->NB = int(NB);
+  return SPADE_OK;
+}
+
+spade_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return SPADE_OK;
+  return fail(SPADE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* spade_status_string(spade_status s) {
+  switch (s) {
+    case SPADE_OK: return "SPADE_OK";
+    case SPADE_ERR_INVALID_ARG: return "SPADE_ERR_INVALID_ARG";
+    case SPADE_ERR_UNSUPPORTED: return "SPADE_ERR_UNSUPPORTED";
+    case SPADE_ERR_WORKSPACE: return "SPADE_ERR_WORKSPACE";
+    case SPADE_ERR_HIP: return "SPADE_ERR_HIP";
+  }
+  return "SPADE_ERR_UNKNOWN";
+}
+
+const char* spade_last_error(void) { return g_last_error; }
+
+spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y, int32_t dtype,
+                                 int32_t inverse, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (dtype != SPADE_BF16 && dtype != SPADE_FP32)
+    return fail(SPADE_ERR_INVALID_ARG, "dtype must be SPADE_BF16 or SPADE_FP32 (got %d)", dtype);
+  if (inverse != 0 && inverse != 1)
+    return fail(SPADE_ERR_INVALID_ARG, "inverse must be 0 or 1 (got %d)", inverse);
+  if (empty) return SPADE_OK;
+  if (!x || !y) return fail(SPADE_ERR_INVALID_ARG, "x and y must be non-null");
+  if (!aligned16(x) || !aligned16(y))
+    return fail(SPADE_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
+  if (x == y) return fail(SPADE_ERR_INVALID_ARG, "x and y must not alias");
+  const int esize = dtype == SPADE_BF16 ? 2 : 4;
+  return hip_status(spade::launch_reorder(dg, x, y, esize, inverse, stream), "reorder launch");
+}
+
+spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb, double* qbar,
+                             double* kbar, double* sics_q, double* sics_k, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if ((sics_q == nullptr) != (sics_k == nullptr))
+    return fail(SPADE_ERR_INVALID_ARG, "sics_q and sics_k must both be given or both be null");
+  if (empty) return SPADE_OK;
+  if (!qb || !kb || !qbar || !kbar)
+    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, qbar and kbar must be non-null");
+  if (!aligned16(qb) || !aligned16(kb) || !aligned16(qbar) || !aligned16(kbar))
+    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, qbar and kbar must be 16-byte aligned");
+  return hip_status(spade::launch_summarize(dg, qb, kb, qbar, kbar, sics_q, sics_k, stream),
+                    "summarize launch");
+}
+
+spade_status spade_estimate_select(const spade_geom* g, const double* qbar, const double* kbar,
+                                   int32_t mode, int32_t topk, double tau, double scale,
+                                   int32_t* counts, int32_t* indices, double* scores,
+                                   hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (mode != SPADE_TOPK && mode != SPADE_TOPP)
+    return fail(SPADE_ERR_INVALID_ARG, "mode must be SPADE_TOPK or SPADE_TOPP (got %d)", mode);
+  if (mode == SPADE_TOPK && topk < 1)
+    return fail(SPADE_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", topk);
+  if (mode == SPADE_TOPP && !(tau > 0.0 && tau <= 1.0))
+    return fail(SPADE_ERR_INVALID_ARG, "tau must lie in (0, 1] (got %g)", tau);
+  if (!(isfinite(scale) && scale > 0.0))
+    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
+  if (!empty && dg.NB > spade::kMaxSelectNB)
+    return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the selection limit %d", dg.NB,
+                spade::kMaxSelectNB);
+  if (empty) return SPADE_OK;
+  if (!qbar || !kbar || !counts || !indices)
+    return fail(SPADE_ERR_INVALID_ARG, "qbar, kbar, counts and indices must be non-null");
+  if (!aligned16(qbar) || !aligned16(kbar))
+    return fail(SPADE_ERR_INVALID_ARG, "qbar and kbar must be 16-byte aligned");
+  return hip_status(spade::launch_estimate_select(dg, qbar, kbar, mode, topk, tau, scale, counts,
+                                                  indices, scores, stream),
+                    "estimate_select launch");
+}
+
+size_t spade_attn_workspace_bytes(const spade_geom* g) {
+  spade::DevGeom dg;
+  bool empty = false;
+  if (check_geom(g, &dg, &empty) != SPADE_OK || empty) return 0;
+  return spade::attn_workspace_bytes(dg);
+}
+
+spade_status spade_block_sparse_attn(const spade_geom* g, const void* qb, const void* kb,
+                                     const void* vb, const int32_t* counts,
+                                     const int32_t* indices, double scale, void* ob, float* lse,
+                                     void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (!(isfinite(scale) && scale > 0.0))
+    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
+  if (empty) return SPADE_OK;
+  if (!qb || !kb || !vb || !counts || !indices || !ob)
+    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, vb, counts, indices and ob must be non-null");
+  if (!aligned16(qb) || !aligned16(kb) || !aligned16(vb) || !aligned16(ob))
+    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, vb and ob must be 16-byte aligned");
+  const size_t need = spade::attn_workspace_bytes(dg);
+  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace_bytes);
+  return hip_status(spade::launch_block_sparse_attn(dg, qb, kb, vb, counts, indices, float(scale),
+                                                    ob, lse, workspace, stream),
+                    "block_sparse_attn launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,59 @@
+// Internal declarations shared by the C-ABI layer and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spade {
+
+// Geometry with the derived block-grid sizes, passed to kernels by value.
+struct DevGeom {
+  int B, H, d;
+  int T, Hs, Ws;
+  int bt, bh, bw;
+  int nT, nH, nW;
+  int NB, BS;
+  int64_t N;
+};
+
+// Origin, per-axis extent and real-token count of block b (T-major block order).
+struct BlockExt {
+  int t0, y0, x0;
+  int et, eh, ew;
+  int n;
+};
+
+__device__ __forceinline__ BlockExt block_ext(const DevGeom& g, int b) {
+  const int wb = b % g.nW;
+  const int r = b / g.nW;
+  const int hb = r % g.nH;
+  const int tb = r / g.nH;
+  BlockExt e;
+  e.t0 = tb * g.bt;
+  e.y0 = hb * g.bh;
+  e.x0 = wb * g.bw;
+  e.et = min(g.bt, g.T - e.t0);
+  e.eh = min(g.bh, g.Hs - e.y0);
+  e.ew = min(g.bw, g.Ws - e.x0);
+  e.n = e.et * e.eh * e.ew;
+  return e;
+}
+
+// Launchers (each returns hipGetLastError() after its launches).
+hipError_t launch_reorder(const DevGeom& g, const void* x, void* y, int esize, int inverse,
+                          hipStream_t s);
+hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
+                            double* kbar, double* sics_q, double* sics_k, hipStream_t s);
+hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const double* kbar,
+                                  int mode, int topk, double tau, double scale, int* counts,
+                                  int* indices, double* scores, hipStream_t s);
+size_t attn_workspace_bytes(const DevGeom& g);
+hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
+                                    const void* vb, const int* counts, const int* indices,
+                                    float scale, void* ob, float* lse, void* ws,
+                                    hipStream_t s);
+
+constexpr int kMaxBS = 256;        // attention: one wave per 32 query rows, <= 8 waves
+constexpr int kMaxSelectNB = 1024;  // selection: one row of scores per wave in registers
+
+}  // namespace spade

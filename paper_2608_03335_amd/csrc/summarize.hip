@@ -1,0 +1,128 @@
+// Summarizer (block mean, paper §3.1 MEAN-SPADE) and intra-block estimator SICS
+// (§3.2, Eq. (4)-(5), Alg. 1) over the blocked bf16 layout.
+//
+// One workgroup per (block, head) reads that block's Q rows, then its K rows.
+// Lane layout: V = d/8 lanes share one token row (16 bytes = 8 bf16 each), so
+// 256/V rows are in flight per pass; every lane accumulates its 8 columns in
+// fp64 and the row groups are combined through LDS in a fixed order.
+//
+// SICS is evaluated in the closed form |sum_k q_k/|q_k||^2, which equals the sum
+// of all pairwise cosines of Eq. (4) (expanding the square gives Eq. (5)'s
+// diagonal plus twice the off-diagonal sum, the quantity Alg. 1 accumulates).
+// It needs one row norm per token (a V-lane reduction) and no sequential scan,
+// so all rows of a block proceed in parallel.
+#include "spade_internal.h"
+
+namespace spade {
+namespace {
+
+constexpr int kThreads = 256;
+
+__device__ __forceinline__ void bf16x8_to_f32(const uint4 v, float f[8]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+template <int D, bool SICS>
+__global__ void __launch_bounds__(kThreads) summarize_kernel(DevGeom g, const uint4* __restrict__ qb,
+                                                             const uint4* __restrict__ kb,
+                                                             double* __restrict__ qbar,
+                                                             double* __restrict__ kbar,
+                                                             double* __restrict__ sics_q,
+                                                             double* __restrict__ sics_k) {
+  constexpr int V = D / 8;          // lanes per token row
+  constexpr int G = kThreads / V;   // token rows per pass
+  __shared__ double part[G][D];
+  __shared__ double upart[SICS ? G : 1][SICS ? D : 1];
+  __shared__ double sq[kThreads / 64];
+
+  const int b = blockIdx.x;
+  const int64_t bh = blockIdx.y;
+  const int n = block_ext(g, b).n;
+  const int vec = threadIdx.x % V, grp = threadIdx.x / V;
+  const int64_t row0 = (bh * g.NB + b) * int64_t(g.BS);
+
+  for (int which = 0; which < 2; ++which) {
+    const uint4* src = (which ? kb : qb) + row0 * V;
+    double acc[8], uacc[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) acc[k] = uacc[k] = 0.0;
+#pragma unroll 2
+    for (int s = grp; s < n; s += G) {
+      float f[8];
+      bf16x8_to_f32(src[int64_t(s) * V + vec], f);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) acc[k] += double(f[k]);
+      if (SICS) {
+        double ss = 0.0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) ss += double(f[k]) * double(f[k]);
+#pragma unroll
+        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
+        const double inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) uacc[k] += double(f[k]) * inv;
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      part[grp][vec * 8 + k] = acc[k];
+      if (SICS) upart[grp][vec * 8 + k] = uacc[k];
+    }
+    __syncthreads();
+    double u2 = 0.0;
+    if (threadIdx.x < D) {
+      const int c = threadIdx.x;
+      double s = 0.0;
+      for (int r = 0; r < G; ++r) s += part[r][c];
+      (which ? kbar : qbar)[(bh * g.NB + b) * D + c] = s / double(n);
+      if (SICS) {
+        double u = 0.0;
+        for (int r = 0; r < G; ++r) u += upart[r][c];
+        u2 = u * u;
+      }
+    }
+    if (SICS) {
+      // sum of u_c^2 over the D columns: wave sums, then a fixed-order total.
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) u2 += __shfl_xor(u2, m, 64);
+      if ((threadIdx.x & 63) == 0) sq[threadIdx.x >> 6] = u2;
+    }
+    __syncthreads();
+    if (SICS && threadIdx.x == 0) {
+      double t = 0.0;
+      for (int w = 0; w < D / 64; ++w) t += sq[w];
+      (which ? sics_k : sics_q)[bh * g.NB + b] = t;
+    }
+    // part/upart/sq are rewritten by the next tensor only after this barrier
+    __syncthreads();
+  }
+}
+
+template <int D>
+hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, double* qbar, double* kbar,
+                    double* sics_q, double* sics_k, hipStream_t s) {
+  const dim3 grid(g.NB, g.B * g.H);
+  const uint4* q = static_cast<const uint4*>(qb);
+  const uint4* k = static_cast<const uint4*>(kb);
+  if (sics_q)
+    summarize_kernel<D, true><<<grid, kThreads, 0, s>>>(g, q, k, qbar, kbar, sics_q, sics_k);
+  else
+    summarize_kernel<D, false><<<grid, kThreads, 0, s>>>(g, q, k, qbar, kbar, nullptr, nullptr);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
+                            double* kbar, double* sics_q, double* sics_k, hipStream_t s) {
+  if (g.d == 128) return launch_d<128>(g, qb, kb, qbar, kbar, sics_q, sics_k, s);
+  if (g.d == 64) return launch_d<64>(g, qb, kb, qbar, kbar, sics_q, sics_k, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace spade

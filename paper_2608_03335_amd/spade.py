@@ -1,0 +1,124 @@
+"""Thin ctypes binding of libspade.so: same names as the C ABI, argument marshalling only.
+
+Tensors are torch tensors used as device buffers; every step of the path runs in
+the library's HIP kernels. Each function raises SpadeError when the library
+returns a non-OK status. Calls are asynchronous on the given HIP stream
+(default: torch's current stream).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspade.so")
+
+SPADE_OK, SPADE_ERR_INVALID_ARG, SPADE_ERR_UNSUPPORTED, SPADE_ERR_WORKSPACE, SPADE_ERR_HIP = range(5)
+SPADE_BF16, SPADE_FP32 = 0, 1
+SPADE_TOPK, SPADE_TOPP = 0, 1
+
+EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_estimate_select",
+            "spade_attn_workspace_bytes", "spade_block_sparse_attn",
+            "spade_status_string", "spade_last_error")
+
+
+class SpadeError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class spade_geom(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("B", "H", "d", "T", "Hs", "Ws", "bt", "bh", "bw")]
+
+    @property
+    def BS(self) -> int:
+        return self.bt * self.bh * self.bw
+
+    @property
+    def NB(self) -> int:
+        return (-(-self.T // self.bt)) * (-(-self.Hs // self.bh)) * (-(-self.Ws // self.bw))
+
+    @property
+    def N(self) -> int:
+        return self.T * self.Hs * self.Ws
+
+
+def geom(B, H, d, T, Hs, Ws, bt, bh, bw) -> spade_geom:
+    return spade_geom(B, H, d, T, Hs, Ws, bt, bh, bw)
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libspade.so; raise if it has not been built (no fallback exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing: build it with "
+                               "`python -m paper_2608_03335_amd.build_lib`")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, i32, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
+        G = ctypes.POINTER(spade_geom)
+        sig = {
+            "spade_block_reorder": (i32, [G, vp, vp, i32, i32, vp]),
+            "spade_summarize": (i32, [G, vp, vp, vp, vp, vp, vp, vp]),
+            "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
+            "spade_attn_workspace_bytes": (sz, [G]),
+            "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
+            "spade_status_string": (ctypes.c_char_p, [i32]),
+            "spade_last_error": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _s(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(status: int):
+    if status != SPADE_OK:
+        L = lib()
+        raise SpadeError(status, f"{L.spade_status_string(status).decode()}: "
+                                 f"{L.spade_last_error().decode()}")
+
+
+def spade_block_reorder(g: spade_geom, x, y, inverse: bool = False, stream=None):
+    dtype = SPADE_BF16 if x.dtype == torch.bfloat16 else SPADE_FP32
+    _check(lib().spade_block_reorder(ctypes.byref(g), _p(x), _p(y), dtype, int(inverse), _s(stream)))
+
+
+def spade_summarize(g: spade_geom, qb, kb, qbar, kbar, sics_q=None, sics_k=None, stream=None):
+    _check(lib().spade_summarize(ctypes.byref(g), _p(qb), _p(kb), _p(qbar), _p(kbar),
+                                 _p(sics_q), _p(sics_k), _s(stream)))
+
+
+def spade_estimate_select(g: spade_geom, qbar, kbar, mode: int, topk: int, tau: float,
+                          scale: float, counts, indices, scores=None, stream=None):
+    _check(lib().spade_estimate_select(ctypes.byref(g), _p(qbar), _p(kbar), int(mode), int(topk),
+                                       float(tau), float(scale), _p(counts), _p(indices),
+                                       _p(scores), _s(stream)))
+
+
+def spade_attn_workspace_bytes(g: spade_geom) -> int:
+    return int(lib().spade_attn_workspace_bytes(ctypes.byref(g)))
+
+
+def spade_block_sparse_attn(g: spade_geom, qb, kb, vb, counts, indices, scale: float, ob,
+                            lse=None, workspace=None, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spade_block_sparse_attn(ctypes.byref(g), _p(qb), _p(kb), _p(vb), _p(counts),
+                                         _p(indices), float(scale), _p(ob), _p(lse),
+                                         _p(workspace), nbytes, _s(stream)))

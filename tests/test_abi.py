@@ -1,0 +1,147 @@
+"""The C-ABI library loads, exports every declared symbol, and rejects bad arguments on the host.
+
+No compute call is made here: every call below fails validation before any HIP
+launch, so these run without a GPU.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_03335_amd import spade as S
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spade.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spade_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_path_calls():
+    names = _declared()
+    for n in ("spade_block_reorder", "spade_summarize", "spade_estimate_select",
+              "spade_block_sparse_attn"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    L = S.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    assert set(_declared()) == set(S.EXPORTED)
+
+
+def _g(**kw):
+    base = dict(B=1, H=2, d=128, T=4, Hs=8, Ws=8, bt=2, bh=4, bw=4)
+    base.update(kw)
+    return S.spade_geom(*[base[k] for k in ("B", "H", "d", "T", "Hs", "Ws", "bt", "bh", "bw")])
+
+
+NULL = None
+FAKE = ctypes.c_void_p(0x1000)      # aligned, never dereferenced (validation fails first)
+MISALIGNED = ctypes.c_void_p(0x1008)
+
+
+def _status(fn, *args):
+    st = fn(*args)
+    msg = S.lib().spade_last_error().decode()
+    return st, msg
+
+
+def test_status_strings():
+    L = S.lib()
+    assert L.spade_status_string(0) == b"SPADE_OK"
+    assert L.spade_status_string(3) == b"SPADE_ERR_WORKSPACE"
+    assert L.spade_status_string(99) == b"SPADE_ERR_UNKNOWN"
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(d=96), S.SPADE_ERR_UNSUPPORTED),
+    (dict(bt=0), S.SPADE_ERR_INVALID_ARG),
+    (dict(B=-1), S.SPADE_ERR_INVALID_ARG),
+    (dict(bt=8, bh=8, bw=8), S.SPADE_ERR_UNSUPPORTED),   # BS = 512 > 256
+])
+def test_geometry_validation(kw, expect):
+    L = S.lib()
+    g = _g(**kw)
+    st, msg = _status(L.spade_block_reorder, ctypes.byref(g), FAKE, FAKE, 0, 0, None)
+    assert st == expect and msg
+
+
+def test_reorder_argument_errors():
+    L = S.lib()
+    g = _g()
+    assert L.spade_block_reorder(None, FAKE, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), NULL, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG  # alias
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, MISALIGNED, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 7, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 0, 2, None) == S.SPADE_ERR_INVALID_ARG
+
+
+def test_empty_problem_is_a_no_op():
+    L = S.lib()
+    for kw in (dict(B=0), dict(H=0), dict(T=0)):
+        g = _g(**kw)
+        assert L.spade_block_reorder(ctypes.byref(g), NULL, NULL, 0, 0, None) == S.SPADE_OK
+        assert L.spade_summarize(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, NULL, None) == S.SPADE_OK
+        assert L.spade_estimate_select(ctypes.byref(g), NULL, NULL, 0, 1, 0.0, 1.0, NULL, NULL, NULL, None) == S.SPADE_OK
+        assert L.spade_attn_workspace_bytes(ctypes.byref(g)) == 0
+        assert L.spade_block_sparse_attn(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, 1.0,
+                                         NULL, NULL, NULL, 0, None) == S.SPADE_OK
+
+
+def test_summarize_errors():
+    L = S.lib()
+    g = _g()
+    assert L.spade_summarize(ctypes.byref(g), FAKE, NULL, FAKE, FAKE, NULL, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_summarize(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("mode,topk,tau,scale,expect", [
+    (2, 1, 0.5, 1.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPK, 0, 0.5, 1.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPP, 1, 0.0, 1.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPP, 1, 1.5, 1.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPP, 1, float("nan"), 1.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPK, 1, 0.5, 0.0, S.SPADE_ERR_INVALID_ARG),
+    (S.SPADE_TOPK, 1, 0.5, float("inf"), S.SPADE_ERR_INVALID_ARG),
+])
+def test_select_parameter_errors(mode, topk, tau, scale, expect):
+    L = S.lib()
+    g = _g()
+    st = L.spade_estimate_select(ctypes.byref(g), FAKE, FAKE, mode, topk, tau, scale, FAKE, FAKE, NULL, None)
+    assert st == expect
+
+
+def test_select_block_count_limit():
+    L = S.lib()
+    g = _g(T=64, Hs=64, Ws=64, bt=2, bh=2, bw=2)  # NB = 32768 > 1024
+    st = L.spade_estimate_select(ctypes.byref(g), FAKE, FAKE, 0, 1, 0.5, 1.0, FAKE, FAKE, NULL, None)
+    assert st == S.SPADE_ERR_UNSUPPORTED
+
+
+def test_attention_workspace_and_pointer_errors():
+    L = S.lib()
+    g = _g()
+    need = L.spade_attn_workspace_bytes(ctypes.byref(g))
+    st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, NULL, FAKE, FAKE, 0.125, FAKE,
+                                   NULL, FAKE, need, None)
+    assert st == S.SPADE_ERR_INVALID_ARG
+    if need > 0:
+        st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE,
+                                       NULL, FAKE, need - 1, None)
+        assert st == S.SPADE_ERR_WORKSPACE
+    st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, -1.0, FAKE,
+                                   NULL, FAKE, need, None)
+    assert st == S.SPADE_ERR_INVALID_ARG
+
+
+def test_python_binding_raises_with_message():
+    g = _g(d=96)
+    with pytest.raises(S.SpadeError, match="head dim"):
+        S._check(S.lib().spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None))

@@ -1,0 +1,270 @@
+"""GPU parity: every C-ABI call against the fp64 oracle on the same seeded bf16 inputs.
+
+Bars: reorder bit-exact; summaries to fp64 rounding; selections exact except
+blocks within 1e-6 (relative) of a row's cut; attention within 2e-2 max-abs,
+run on the oracle's own block lists so selection and attention are checked
+independently.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from gen.workloads import workload
+from oracle import spade_oracle as O
+from paper_2608_03335_amd import spade as S
+from paper_2608_03335_amd.pipeline import SpadePath
+
+from . import _parity as P
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _case(name):
+    if name == "tiny":
+        return workload("tiny")
+    table = {
+        "ragged_d64": dict(T=5, Hs=7, Ws=9, bt=2, bh=3, bw=4, d=64, H=3),      # BS 24, 1 wave
+        "ragged_d128": dict(T=6, Hs=11, Ws=13, bt=3, bh=4, bw=5, d=128, H=2),  # BS 60, 2 waves
+        "bs144_tail": dict(T=6, Hs=12, Ws=20, bt=3, bh=6, bw=8, d=128, H=2),   # BS 144: 5th wave half empty
+        "bs256_max": dict(T=8, Hs=16, Ws=12, bt=4, bh=8, bw=8, d=128, H=1),    # BS 256: 8 waves
+        "one_token": dict(T=1, Hs=1, Ws=1, bt=1, bh=1, bw=1, d=64, H=2),       # NB = BS = N = 1
+        "one_block": dict(T=3, Hs=5, Ws=7, bt=4, bh=8, bw=8, d=128, H=2),      # a single padded block
+    }
+    kw = dict(table[name])
+    return P.small_cfg(kw.pop("T"), kw.pop("Hs"), kw.pop("Ws"), kw.pop("bt"), kw.pop("bh"),
+                       kw.pop("bw"), **kw)
+
+
+SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block"]
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _geom(cfg):
+    return S.geom(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"],
+                  cfg["bh"], cfg["bw"])
+
+
+def _path(cfg, **kw):
+    opts = dict(mode=cfg["mode"], topk=cfg.get("topk"), tau=cfg.get("tau"), device=DEV)
+    opts.update(kw)
+    return SpadePath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"],
+                     cfg["bh"], cfg["bw"], **opts)
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_reorder_bit_exact(name):
+    cfg = _case(name)
+    _say("reorder", name)
+    g, og = _geom(cfg), P.geometry(cfg)
+    Q, _, _ = P.bf16_inputs(cfg)
+    for x in (Q, Q.float()):
+        xb = torch.full((cfg["B"], cfg["H"], g.NB * g.BS, cfg["d"]), float("nan"), dtype=x.dtype, device=DEV)
+        S.spade_block_reorder(g, x, xb)
+        back = torch.full_like(x, float("nan"))
+        S.spade_block_reorder(g, xb, back, inverse=True)
+        torch.cuda.synchronize()
+        iview = torch.int16 if x.dtype == torch.bfloat16 else torch.int32
+        ref = O.reorder(x.view(iview).cpu().numpy(), og)
+        assert np.array_equal(xb.view(iview).cpu().numpy(), ref)
+        assert torch.equal(back.view(iview), x.view(iview))
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_summaries(name):
+    cfg = _case(name)
+    _say("summaries", name)
+    p = _path(cfg, with_sics=True)
+    og = P.geometry(cfg)
+    Q, K, V = P.bf16_inputs(cfg)
+    p.reorder_in(Q, K, V)
+    p.summarize()
+    torch.cuda.synchronize()
+    for X, xbar, sics in ((Q, p.qbar, p.sics_q), (K, p.kbar, p.sics_k)):
+        Xb = O.reorder(P.to_np64(X), og)
+        ref = O.block_means(Xb, og)
+        got = xbar.cpu().numpy()
+        assert np.max(np.abs(got - ref)) <= 1e-12 * (1 + np.max(np.abs(ref)))
+        ref_s = O.block_sics(Xb, og, "closed")
+        np.testing.assert_allclose(sics.cpu().numpy(), ref_s, rtol=1e-9, atol=1e-9)
+
+
+def _oracle_selection(cfg, Q, K, mode, topk=None, tau=None):
+    og = P.geometry(cfg)
+    qbar = O.block_means(O.reorder(P.to_np64(Q), og), og)
+    kbar = O.block_means(O.reorder(P.to_np64(K), og), og)
+    s = O.block_scores(qbar, kbar, P.scale_of(cfg["d"]))
+    c, i = O.select(s, mode, topk=topk, tau=tau)
+    return s, c, i
+
+
+RULES = [("topk", 1, None), ("topk", 3, None), ("topk", 10 ** 6, None),
+         ("topp", None, 0.5), ("topp", None, 0.9), ("topp", None, 1.0)]
+
+
+@pytest.mark.parametrize("rule", RULES, ids=lambda r: f"{r[0]}-{r[1] or r[2]}")
+@pytest.mark.parametrize("name", SMALL)
+def test_selection(name, rule):
+    mode, k, tau = rule
+    cfg = _case(name)
+    _say("selection", name, rule)
+    p = _path(cfg, mode=mode, topk=k, tau=tau)
+    Q, K, V = P.bf16_inputs(cfg)
+    p.reorder_in(Q, K, V)
+    p.summarize()
+    scores = torch.empty((cfg["B"], cfg["H"], p.g.NB, p.g.NB), dtype=torch.float64, device=DEV)
+    S.spade_estimate_select(p.g, p.qbar, p.kbar, p.mode, p.topk, p.tau, p.scale, p.counts,
+                            p.indices, scores)
+    torch.cuda.synchronize()
+    s, c, i = _oracle_selection(cfg, Q, K, mode, k, tau)
+    np.testing.assert_allclose(scores.cpu().numpy(), s, rtol=1e-12, atol=1e-12)
+    P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(), mode, tau)
+
+
+def _attention_vs_oracle(cfg, p, Q, K, V, counts, indices, rows=None):
+    og = P.geometry(cfg)
+    ci = torch.from_numpy(counts).to(DEV)
+    ii = torch.from_numpy(indices).to(DEV)
+    p.reorder_in(Q, K, V)
+    p.attend(ci, ii)
+    torch.cuda.synchronize()
+    Qb, Kb, Vb = (O.reorder(P.to_np64(x), og) for x in (Q, K, V))
+    ref, ref_lse = O.block_sparse_attention(Qb, Kb, Vb, counts, indices, og, P.scale_of(cfg["d"]),
+                                            rows=rows)
+    got = P.to_np64(p.Ob)
+    got_lse = p.lse.cpu().numpy().astype(np.float64) if p.lse is not None else None
+    slot_token, nv = O.block_tables(og)
+    BS = og.BS
+    worst = 0.0
+    todo = rows if rows is not None else [(b, h, i) for b in range(cfg["B"]) for h in range(cfg["H"])
+                                          for i in range(og.NB)]
+    for (b, h, i) in todo:
+        sl = slice(i * BS, i * BS + nv[i])
+        err = np.max(np.abs(got[b, h, sl] - ref[b, h, sl]))
+        worst = max(worst, err)
+        assert np.all(got[b, h, i * BS + nv[i]:(i + 1) * BS] == 0), "padding slots must be 0"
+        if got_lse is not None:
+            np.testing.assert_allclose(got_lse[b, h, sl], ref_lse[b, h, sl], rtol=0, atol=1e-3)
+    return worst
+
+
+@pytest.mark.parametrize("name", SMALL)
+def test_attention_on_oracle_mask(name):
+    cfg = _case(name)
+    _say("attention", name)
+    Q, K, V = P.bf16_inputs(cfg)
+    mode, k, tau = ("topk", 3, None) if cfg["mode"] == "topk" else ("topp", None, 0.9)
+    _, c, i = _oracle_selection(cfg, Q, K, mode, k, tau)
+    p = _path(cfg, with_lse=True)
+    worst = _attention_vs_oracle(cfg, p, Q, K, V, c, i)
+    _say(f"  max-abs {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
+
+
+@pytest.mark.parametrize("name", ["tiny", "ragged_d64", "ragged_d128", "one_block"])
+def test_all_kept_equals_dense(name):
+    """A full mask through the sparse kernel equals dense attention, Eq. (1)."""
+    cfg = _case(name)
+    _say("dense", name)
+    og = P.geometry(cfg)
+    Q, K, V = P.bf16_inputs(cfg)
+    NB = og.NB
+    counts = np.full((cfg["B"], cfg["H"], NB), NB, np.int32)
+    idx = np.broadcast_to(np.arange(NB, dtype=np.int32), (cfg["B"], cfg["H"], NB, NB)).copy()
+    p = _path(cfg)
+    p.reorder_in(Q, K, V)
+    p.attend(torch.from_numpy(counts).to(DEV), torch.from_numpy(idx).to(DEV))
+    p.restore()
+    torch.cuda.synchronize()
+    ref = O.dense_attention(P.to_np64(Q), P.to_np64(K), P.to_np64(V), P.scale_of(cfg["d"]))
+    assert np.max(np.abs(P.to_np64(p.O) - ref)) <= P.ATTN_MAX_ABS
+
+
+def test_malformed_lists_are_clamped_and_skipped():
+    cfg = _case("ragged_d128")
+    og = P.geometry(cfg)
+    NB = og.NB
+    Q, K, V = P.bf16_inputs(cfg)
+    _, c, i = _oracle_selection(cfg, Q, K, "topk", 3)
+    c2, i2 = c.copy(), np.full_like(i, -1)
+    # row 0: a zero count; row 1: out-of-range entries around the real ones;
+    # row 2: count above NB with trailing garbage
+    c2[0, 0, 0] = 0
+    i2[0, 0, 1, :5] = [-7, i[0, 0, 1, 0], NB + 3, i[0, 0, 1, 1], i[0, 0, 1, 2]]
+    c2[0, 0, 1] = 5
+    c2[0, 0, 2] = NB + 100
+    i2[0, 0, 2, : c[0, 0, 2]] = i[0, 0, 2, : c[0, 0, 2]]
+    for r in range(3, NB):
+        i2[0, 0, r] = i[0, 0, r]
+    i2[:, 1:] = i[:, 1:]
+    p = _path(cfg, with_lse=True)
+    p.reorder_in(Q, K, V)
+    p.attend(torch.from_numpy(c2).to(DEV), torch.from_numpy(i2).to(DEV))
+    torch.cuda.synchronize()
+    got = P.to_np64(p.Ob)
+    lse = p.lse.cpu().numpy()
+    BS = og.BS
+    _, nv = O.block_tables(og)
+    assert np.all(got[0, 0, :BS] == 0) and np.all(np.isneginf(lse[0, 0, : nv[0]]))
+    Qb, Kb, Vb = (O.reorder(P.to_np64(x), og) for x in (Q, K, V))
+    ref, _ = O.block_sparse_attention(Qb, Kb, Vb, c, i, og, P.scale_of(cfg["d"]),
+                                      rows=[(0, 0, 1), (0, 0, 2)])
+    for r in (1, 2):
+        sl = slice(r * BS, r * BS + nv[r])
+        assert np.max(np.abs(got[0, 0, sl] - ref[0, 0, sl])) <= P.ATTN_MAX_ABS
+
+
+def test_attention_is_deterministic():
+    cfg = _case("bs144_tail")
+    Q, K, V = P.bf16_inputs(cfg)
+    p = _path(cfg)
+    p.run(Q, K, V)
+    first = p.O.clone()
+    p.run(Q, K, V)
+    torch.cuda.synchronize()
+    assert torch.equal(first.view(torch.int16), p.O.view(torch.int16))
+
+
+# ---------------- full attention-layer shapes, bench launch configuration ----------------
+@pytest.mark.parametrize("name,n_rows", [("wan13b", 24), ("hunyuan", 24)])
+def test_full_shape_pipeline(name, n_rows):
+    cfg = workload(name)
+    _say("full", name)
+    og = P.geometry(cfg)
+    Q, K, V = P.bf16_inputs(cfg)
+    p = _path(cfg, with_lse=True)
+    p.run(Q, K, V)
+    torch.cuda.synchronize()
+    # selection: oracle on the same bf16 inputs, every row
+    s, c, i = _oracle_selection(cfg, Q, K, cfg["mode"], cfg.get("topk"), cfg.get("tau"))
+    n_ex = P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(),
+                               cfg["mode"], cfg.get("tau"))
+    _say(f"  selection rows exempt: {n_ex}; block sparsity {O.block_sparsity(c, og.NB):.4f}")
+    # attention: sampled query blocks (incl. first/last) recomputed by the oracle with the
+    # GPU's own lists (identical to the oracle's outside exempt rows)
+    cg, ig = p.counts.cpu().numpy(), p.indices.cpu().numpy()
+    rows = P.sample_rows(cfg["B"], cfg["H"], og.NB, n_rows, seed=1,
+                         must=[(0, 0, 0), (0, cfg["H"] - 1, og.NB - 1)])
+    Qb, Kb, Vb = (O.reorder(P.to_np64(x), og) for x in (Q, K, V))
+    # restrict the blocked copies to sampled heads to bound host memory
+    ref, ref_lse = O.block_sparse_attention(Qb, Kb, Vb, cg, ig, og, P.scale_of(cfg["d"]), rows=rows)
+    got = P.to_np64(p.Ob)
+    O_raster = P.to_np64(p.O)
+    pos = O.token_position(og)
+    _, nv = O.block_tables(og)
+    worst = 0.0
+    for (b, h, i) in rows:
+        sl = slice(i * og.BS, i * og.BS + nv[i])
+        worst = max(worst, float(np.max(np.abs(got[b, h, sl] - ref[b, h, sl]))))
+        np.testing.assert_allclose(p.lse.cpu().numpy()[b, h, sl], ref_lse[b, h, sl], atol=1e-3, rtol=0)
+    # restore layer: the raster output is the inverse permutation of the blocked one
+    assert np.array_equal(O_raster, got[:, :, pos])
+    _say(f"  attention max-abs over {len(rows)} sampled query blocks: {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
