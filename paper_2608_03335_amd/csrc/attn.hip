@@ -2,20 +2,27 @@
 //
 // One workgroup per query block (b, h, i); wave w owns query slots 32w..32w+31.
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
-// chunks of 32 key slots (only chunks that contain real keys). Each chunk is
-// staged in LDS, double-buffered: while the waves run MFMA on chunk c, the
-// next chunk's K and V are already in flight from HBM into registers.
+// chunks of 32 key slots (only chunks that hold real keys).
 //
-// Transposed formulation so that every softmax statistic is per lane:
-//   S^T (32 keys x 32 queries) = K_chunk * Q^T   v_mfma_f32_32x32x16_bf16, d/16 steps
-//   lane l then holds query row l%32 and 16 of the chunk's keys;
-//   O^T (d x 32 queries) += V^T * P^T            P^T taken straight from the
-//   S^T accumulators (rounded to bf16) as the B operand; the key order of the
-//   contraction is permuted to match the accumulator layout, and V^T is laid
-//   out in LDS so each lane reads two 8-byte runs of 4 keys.
-// Row max needs one cross-lane exchange (lane l <-> l^32); the row sum is kept
-// per lane and combined once at the end. Logits are scaled into base 2 so the
-// exponentials are single v_exp_f32 instructions.
+// Data movement: each chunk's K and V rows go straight from HBM into LDS with
+// 16-byte global_load_lds (no register staging), double-buffered so chunk c+1
+// is in flight while chunk c is computed. Rows are stored unpadded with the
+// 16-byte pieces XOR-swizzled per row, which keeps both LDS read patterns below
+// free of bank conflicts. Key slots past a block's real tokens re-read the
+// block's last real row (finite data; their logits are masked).
+//
+// Math, transposed so every softmax statistic is per lane:
+//   S^T (32 keys x 32 queries) = K * Q^T        v_mfma_f32_32x32x16_bf16, d/16 steps;
+//     lane l then holds query row l%32 and 16 keys of the chunk.
+//   O^T (d x 32 queries) += V^T * P^T           P^T straight from the S^T registers
+//     (rounded to bf16) as the B operand; the contraction's key order follows the
+//     accumulator layout, and ds_read_b64_tr_b16 delivers V^T fragments in that
+//     order from row-major V.
+// Softmax: logits are scaled into base 2 (one FMA + v_exp_f32 per element); the
+// row max pairs lanes l and l^32 with v_permlane32_swap; the running max is only
+// raised (and O rescaled) when some row's max grows by more than 2^8, so most
+// chunks skip the 64-register rescale; row sums use bf16 dot2 on the same packed
+// P that feeds the MFMA.
 #include "spade_internal.h"
 
 namespace spade {
@@ -23,21 +30,30 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
-constexpr int kChunk = 32;  // key slots per chunk
+constexpr int kChunk = 32;          // key slots per chunk
+constexpr float kRescaleLog2 = 8.0f;  // lazy-rescale threshold (base-2 logits)
 
 template <int D>
 struct Tile {
-  static constexpr int KROW = D + 8;         // K rows, bf16 elements (16-byte pad)
-  static constexpr int VROW = kChunk + 8;    // V^T rows (one per d), bf16 elements
-  static constexpr int K_ELEMS = kChunk * KROW;
-  static constexpr int V_ELEMS = D * VROW;
-  static constexpr int BUF = K_ELEMS + V_ELEMS;
-  static constexpr int ROW_VEC = D / 8;      // 16-byte vectors per token row
-  static constexpr int K_LOADS = kChunk * ROW_VEC;      // 16-byte K loads per chunk
-  static constexpr int V_UNITS = (kChunk / 4) * ROW_VEC;  // 4 keys x 8 d per unit
+  static constexpr int NCH = D / 8;                 // 16-byte pieces per row
+  static constexpr int ROW_BYTES = D * 2;
+  static constexpr int TILE_BYTES = kChunk * ROW_BYTES;
+  static constexpr int RPI = 64 / NCH;              // rows per wave-wide 1 KB load
+  static constexpr int LOADS = kChunk / RPI;        // wave loads per tile
+  static constexpr int BUF_BYTES = 2 * TILE_BYTES;  // K tile then V tile
 };
+
+// swizzles: LDS piece c of tile row r holds global piece c ^ f(r)
+template <int D>
+__device__ __forceinline__ int swz_k(int r) { return r & (Tile<D>::NCH - 1); }
+__device__ __forceinline__ int swz_v(int r) { return 2 * (r & 3); }
 
 // Position in the kept-block walk: list entry jj, its block j and real-key count nj,
 // and the chunk's first key slot c0.
@@ -65,17 +81,37 @@ __device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const int* list, 
   return c;
 }
 
+// Issue this wave's share of the 16-byte global->LDS loads of one chunk.
+template <int D, int W>
+__device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, const char* vb,
+                                           int64_t head_row, const Cursor& c, lds_char* buf,
+                                           int wave, int lane) {
+  using TL = Tile<D>;
+  const int64_t blk_row = head_row + int64_t(c.j) * g.BS + c.c0;
+  const int last = c.nj - 1 - c.c0;  // last real key slot of the chunk
+  const int piece = lane % TL::NCH;
+#pragma unroll
+  for (int q = wave; q < 2 * TL::LOADS; q += W) {
+    const bool is_v = q >= TL::LOADS;
+    const int qq = is_v ? q - TL::LOADS : q;
+    const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
+    const int src_r = min(r, last);
+    const int gp = piece ^ (is_v ? swz_v(r) : swz_k<D>(r));
+    const char* src = (is_v ? vb : kb) + (blk_row + src_r) * TL::ROW_BYTES + gp * 16;
+    lds_char* dst = buf + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
+    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)dst, 16, 0, 0);
+  }
+}
+
 template <int D, int W>
 __global__ void __launch_bounds__(64 * W)
-    attn_kernel(DevGeom g, const uint4* __restrict__ qb, const uint4* __restrict__ kb,
-                const uint4* __restrict__ vb, const int* __restrict__ counts,
+    attn_kernel(DevGeom g, const uint4* __restrict__ qb, const char* __restrict__ kb,
+                const char* __restrict__ vb, const int* __restrict__ counts,
                 const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
                 float* __restrict__ lse) {
   using TL = Tile<D>;
-  constexpr int NT = 64 * W;
-  constexpr int KL = (TL::K_LOADS + NT - 1) / NT;
-  constexpr int VU = (TL::V_UNITS + NT - 1) / NT;
-  __shared__ __align__(16) __bf16 lds[2][TL::BUF];
+  __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
+  lds_char* const lds = (lds_char*)lds_raw;
 
   const int64_t item = blockIdx.x;
   const int64_t bh = item / g.NB;
@@ -91,7 +127,7 @@ __global__ void __launch_bounds__(64 * W)
   bf16x8 qf[D / 16];
   {
     const int qs = q0 + r32;
-    const uint4* src = qb + (head_row + int64_t(i) * g.BS + qs) * TL::ROW_VEC + half;
+    const uint4* src = qb + (head_row + int64_t(i) * g.BS + qs) * TL::NCH + half;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -103,67 +139,15 @@ __global__ void __launch_bounds__(64 * W)
   const int cnt = min(max(counts[bh * g.NB + i], 0), g.NB);
   const int* list = indices + (bh * g.NB + i) * int64_t(g.NB);
 
-  uint4 kreg[KL];
-  uint4 vreg[VU][4];
-  auto load_chunk = [&](const Cursor& c) {
-    const int64_t base = head_row + int64_t(c.j) * g.BS + c.c0;  // first key row of the chunk
-#pragma unroll
-    for (int u = 0; u < KL; ++u) {
-      const int f = tid + u * NT;
-      kreg[u] = make_uint4(0, 0, 0, 0);
-      if (f < TL::K_LOADS) {
-        const int key = f / TL::ROW_VEC, vec = f % TL::ROW_VEC;
-        if (c.c0 + key < c.nj) kreg[u] = kb[(base + key) * TL::ROW_VEC + vec];
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int f = tid + u * NT;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) vreg[u][r] = make_uint4(0, 0, 0, 0);
-      if (f < TL::V_UNITS) {
-        const int kq = f % (kChunk / 4), dq = f / (kChunk / 4);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int key = 4 * kq + r;
-          if (c.c0 + key < c.nj) vreg[u][r] = vb[(base + key) * TL::ROW_VEC + dq];
-        }
-      }
-    }
-  };
-  auto store_chunk = [&](__bf16* buf) {
-#pragma unroll
-    for (int u = 0; u < KL; ++u) {
-      const int f = tid + u * NT;
-      if (f < TL::K_LOADS) {
-        const int key = f / TL::ROW_VEC, vec = f % TL::ROW_VEC;
-        *reinterpret_cast<uint4*>(buf + key * TL::KROW + vec * 8) = kreg[u];
-      }
-    }
-    __bf16* vt = buf + TL::K_ELEMS;
-#pragma unroll
-    for (int u = 0; u < VU; ++u) {
-      const int f = tid + u * NT;
-      if (f < TL::V_UNITS) {
-        const int kq = f % (kChunk / 4), dq = f / (kChunk / 4);
-        // vreg[u][r] holds V[key 4kq+r][d 8dq .. 8dq+7]; write V^T rows d, keys 4kq..4kq+3
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint32_t lo = 0, hi = 0;
-          const int sh = (e & 1) * 16;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const uint32_t w = (e >> 1) == 0 ? vreg[u][r].x : (e >> 1) == 1 ? vreg[u][r].y
-                             : (e >> 1) == 2 ? vreg[u][r].z : vreg[u][r].w;
-            const uint32_t h16 = (w >> sh) & 0xffffu;
-            if (r < 2) lo |= h16 << (16 * r);
-            else hi |= h16 << (16 * (r - 2));
-          }
-          *reinterpret_cast<uint2*>(vt + (8 * dq + e) * TL::VROW + 4 * kq) = make_uint2(lo, hi);
-        }
-      }
-    }
-  };
+  // per-lane LDS byte offsets that do not depend on the chunk
+  // K operand: tile row r32, global piece 2*kk + half
+  const int k_off = r32 * TL::ROW_BYTES;
+  const int k_sw = swz_k<D>(r32);
+  // V^T operand via transposing reads: 16-lane group G, index s
+  const int G = lane >> 4, s16 = lane & 15;
+  const int v_row0 = 4 * (G >> 1) + (s16 >> 2);     // + 16u + 8h
+  const int v_piece0 = 2 * (G & 1) + ((s16 & 3) >> 1);  // + 4t
+  const int v_sub = (s16 & 1) * 8;
 
   f32x16 o[D / 32];
 #pragma unroll
@@ -172,79 +156,96 @@ __global__ void __launch_bounds__(64 * W)
     for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
   float m = -INFINITY, l = 0.0f;
   const bool rows_live = q0 < n_i;
+  const bf16x2 ones = {__bf16(1.0f), __bf16(1.0f)};
 
-  Cursor cur = {-1, 0, 0, 0};
-  cur.c0 = -kChunk;  // so that next_chunk starts at list entry 0, slot 0
+  Cursor cur = {-1, 0, 0, -kChunk};
   cur = next_chunk(g, list, cnt, cur);
   int buf = 0;
-  if (cur.jj < cnt) {
-    load_chunk(cur);
-    store_chunk(lds[0]);
-  }
+  if (cur.jj < cnt) load_chunk<D, W>(g, kb, vb, head_row, cur, lds, wave, lane);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   while (cur.jj < cnt) {
     const Cursor nxt = next_chunk(g, list, cnt, cur);
-    const bool more = nxt.jj < cnt;
-    if (more) load_chunk(nxt);
+    if (nxt.jj < cnt) load_chunk<D, W>(g, kb, vb, head_row, nxt, lds + (buf ^ 1) * TL::BUF_BYTES, wave, lane);
     if (rows_live) {
-      const __bf16* K = lds[buf];
-      const __bf16* Vt = lds[buf] + TL::K_ELEMS;
+      lds_char* Kt = lds + buf * TL::BUF_BYTES;
+      lds_char* Vt = Kt + TL::TILE_BYTES;
       f32x16 s;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.0f;
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(K + r32 * TL::KROW + 16 * kk + 8 * half);
+        const bf16x8 a = *(lds_bf16x8*)(Kt + k_off + (((2 * kk + half) ^ k_sw) << 4));
         s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
       }
       // s[r]: key (r/4)*8 + 4*half + r%4 of the chunk, query row r32
-      float mloc = -INFINITY;
+      if (cur.c0 + kChunk > cur.nj) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kr = (r >> 2) * 8 + 4 * half + (r & 3);
-        const float v = (cur.c0 + kr < cur.nj) ? s[r] * scale_log2 : -INFINITY;
-        s[r] = v;
-        mloc = fmaxf(mloc, v);
+        for (int r = 0; r < 16; ++r) {
+          const int kr = (r >> 2) * 8 + 4 * half + (r & 3);
+          if (cur.c0 + kr >= cur.nj) s[r] = -INFINITY;
+        }
       }
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float mnew = fmaxf(m, mloc);
-      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
-      float psum = 0.0f;
+      float mx = s[0];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] = __builtin_amdgcn_exp2f(s[r] - mnew);
-        psum += s[r];
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
       }
-      l = l * alpha + psum;
-      m = mnew;
+      if (__any(mx > m + kRescaleLog2)) {
+        const float mnew = fmaxf(m, mx);
+        const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+        l *= alpha;
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+        m = mnew;
+      }
       bf16x8 p[2];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        p[0][e] = __bf16(s[e]);
-        p[1][e] = __bf16(s[8 + e]);
+      for (int r = 0; r < 16; ++r) {
+        const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(s[r], scale_log2, -m));
+        p[r >> 3][r & 7] = __bf16(e);
       }
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 pr = {p[u][2 * e], p[u][2 * e + 1]};
+          l = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l, false);
+        }
 #pragma unroll
       for (int t = 0; t < D / 32; ++t) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
-#pragma unroll
         for (int u = 0; u < 2; ++u) {
-          const __bf16* vrow = Vt + (32 * t + r32) * TL::VROW + 16 * u + 4 * half;
-          const bf16x4 lo = *reinterpret_cast<const bf16x4*>(vrow);
-          const bf16x4 hi = *reinterpret_cast<const bf16x4*>(vrow + 8);
-          const bf16x8 a = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+          bf16x4 h2[2];
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int row = 16 * u + 8 * h + v_row0;
+            const int piece = (4 * t + v_piece0) ^ swz_v(row);
+            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
+          }
+          const bf16x8 a = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
           o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[u], o[t], 0, 0, 0);
         }
       }
     }
-    if (more) store_chunk(lds[buf ^ 1]);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     buf ^= 1;
     cur = nxt;
   }
 
   // normalise and store: lane holds query row q0 + r32, d = 32t + 8*rq + 4*half + 0..3
-  l += __shfl_xor(l, 32, 64);
+  {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l),
+                                                     false, false);
+    l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
   const int qs = q0 + r32;
   if (qs < g.BS) {
     const bool real = qs < n_i;
@@ -261,7 +262,7 @@ __global__ void __launch_bounds__(64 * W)
       }
     if (lse && real && half == 0)
       lse[head_row + int64_t(i) * g.BS + qs] =
-          l > 0.0f ? (m + __log2f(l)) * 0.69314718055994530942f : -INFINITY;
+          l > 0.0f ? (m + log2f(l)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 
@@ -271,8 +272,8 @@ hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const voi
                      hipStream_t s) {
   const int64_t items = int64_t(g.B) * g.H * g.NB;
   attn_kernel<D, W><<<dim3(unsigned(items)), 64 * W, 0, s>>>(
-      g, static_cast<const uint4*>(qb), static_cast<const uint4*>(kb),
-      static_cast<const uint4*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
+      g, static_cast<const uint4*>(qb), static_cast<const char*>(kb),
+      static_cast<const char*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
   return hipGetLastError();
 }
 

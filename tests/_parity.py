@@ -11,6 +11,10 @@ from oracle import spade_oracle as O
 
 # Attention parity bar: bf16 inputs, fp32 accumulation, bf16 output.
 ATTN_MAX_ABS = 2e-2
+# Log-sum-exp: the kernel's softmax denominator sums the bf16-rounded weights that
+# also feed the P*V product (relative error <= 2^-9 each, same sign at worst), so
+# |lse - lse_exact| <= log(1 + 2^-9) plus fp32 rounding of the sum; 4e-3 covers it.
+LSE_MAX_ABS = 4e-3
 # Selection: memberships may differ only for blocks whose score lies within this
 # relative distance of the row's cut (or, for Top-P, where the prefix mass at the
 # boundary lies within it of tau).
