@@ -26,7 +26,8 @@
  *     status (no partial work). A launch failure returns SPADE_ERR_HIP. Device
  *     faults surface at the caller's next synchronisation. spade_last_error()
  *     gives a message for the calling thread's most recent failure.
- *   - Limits: d in {64, 128}; BS <= 256; NB <= 1024 for the selection call.
+ *   - Limits: d in {64, 128}; BS <= 256; NB <= 1024 for the selection call and
+ *     NB <= 16384 for the attention call.
  *     B, H, T, Hs or Ws equal to 0 is an empty problem: the call returns
  *     SPADE_OK without launching anything (pointers are then not read).
  */

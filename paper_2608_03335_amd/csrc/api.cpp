@@ -164,6 +164,9 @@ spade_status spade_block_sparse_attn(const spade_geom* g, const void* qb, const 
   if (st != SPADE_OK) return st;
   if (!(isfinite(scale) && scale > 0.0))
     return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
+  if (!empty && dg.NB > spade::kMaxAttnNB)
+    return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the attention limit %d", dg.NB,
+                spade::kMaxAttnNB);
   if (empty) return SPADE_OK;
   if (!qb || !kb || !vb || !counts || !indices || !ob)
     return fail(SPADE_ERR_INVALID_ARG, "qb, kb, vb, counts, indices and ob must be non-null");

@@ -55,5 +55,6 @@ hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void
 
 constexpr int kMaxBS = 256;        // attention: one wave per 32 query rows, <= 8 waves
 constexpr int kMaxSelectNB = 1024;  // selection: one row of scores per wave in registers
+constexpr int kMaxAttnNB = 16384;   // attention: a work item's kept list is staged in LDS
 
 }  // namespace spade

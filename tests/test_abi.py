@@ -125,6 +125,14 @@ def test_select_block_count_limit():
     assert st == S.SPADE_ERR_UNSUPPORTED
 
 
+def test_attention_block_count_limit():
+    L = S.lib()
+    g = _g(T=64, Hs=64, Ws=64, bt=1, bh=2, bw=2)  # NB = 65536 > 16384
+    st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE,
+                                   NULL, FAKE, 0, None)
+    assert st == S.SPADE_ERR_UNSUPPORTED
+
+
 def test_attention_workspace_and_pointer_errors():
     L = S.lib()
     g = _g()
