@@ -6,7 +6,12 @@
 //
 // Data movement: each chunk's K and V rows go straight from HBM into LDS with
 // 16-byte global_load_lds (no register staging), double-buffered so chunk c+1
-// is in flight while chunk c is computed. Rows are stored unpadded with the
+// is in flight while chunk c is computed. The loads are issued from inline asm:
+// the compiler then schedules every LDS read with exact lgkmcnt tracking instead
+// of draining the in-flight LDS-DMA load before each read (it cannot prove the
+// load targets the other buffer); completion is ordered by the explicit wait and
+// barrier at the end of each chunk. The work item's kept list is staged in LDS
+// once, so the walk over kept blocks issues no vector-memory reads. Rows are stored unpadded with the
 // 16-byte pieces XOR-swizzled per row, which keeps both LDS read patterns below
 // free of bank conflicts. Key slots past a block's real tokens re-read the
 // block's last real row (finite data; their logits are masked).
@@ -34,6 +39,7 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) char lds_char;
+typedef __attribute__((address_space(3))) int lds_int;
 typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 typedef __attribute__((address_space(3))) bf16x8 lds_bf16x8;
 
@@ -61,7 +67,7 @@ struct Cursor {
   int jj, j, nj, c0;
 };
 
-__device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const int* list, int cnt,
+__device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const lds_int* list, int cnt,
                                              Cursor c) {
   c.c0 += kChunk;
   while (c.c0 >= c.nj) {
@@ -71,7 +77,7 @@ __device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const int* list, 
       c.c0 = 0;
       return c;
     }
-    const int j = list[c.jj];
+    const int j = __builtin_amdgcn_readfirstlane(list[c.jj]);  // uniform: keep in SGPRs
     if (j >= 0 && j < g.NB) {
       c.j = j;
       c.nj = block_ext(g, j).n;
@@ -98,8 +104,9 @@ __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, con
     const int src_r = min(r, last);
     const int gp = piece ^ (is_v ? swz_v(r) : swz_k<D>(r));
     const char* src = (is_v ? vb : kb) + (blk_row + src_r) * TL::ROW_BYTES + gp * 16;
-    lds_char* dst = buf + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
-    __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)dst, 16, 0, 0);
+    const uint32_t dst =  // M0: LDS base of this wave-wide 1 KB load
+        uint32_t(reinterpret_cast<uintptr_t>(buf)) + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(dst) : "memory");
   }
 }
 
@@ -111,7 +118,9 @@ __global__ void __launch_bounds__(64 * W)
                 float* __restrict__ lse) {
   using TL = Tile<D>;
   __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
+  extern __shared__ int list_raw[];  // kept list of this work item, NB entries
   lds_char* const lds = (lds_char*)lds_raw;
+  lds_int* const list = (lds_int*)list_raw;
 
   const int64_t item = blockIdx.x;
   const int64_t bh = item / g.NB;
@@ -137,7 +146,11 @@ __global__ void __launch_bounds__(64 * W)
   }
 
   const int cnt = min(max(counts[bh * g.NB + i], 0), g.NB);
-  const int* list = indices + (bh * g.NB + i) * int64_t(g.NB);
+  {
+    const int* src = indices + (bh * g.NB + i) * int64_t(g.NB);
+    for (int e = threadIdx.x; e < cnt; e += 64 * W) list[e] = src[e];
+  }
+  __syncthreads();  // list visible to every wave (also completes the Q loads)
 
   // per-lane LDS byte offsets that do not depend on the chunk
   // K operand: tile row r32, global piece 2*kk + half
@@ -271,7 +284,15 @@ hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const voi
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                      hipStream_t s) {
   const int64_t items = int64_t(g.B) * g.H * g.NB;
-  attn_kernel<D, W><<<dim3(unsigned(items)), 64 * W, 0, s>>>(
+  static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       int(kMaxAttnNB * sizeof(int)));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  attn_kernel<D, W><<<dim3(unsigned(items)), 64 * W, size_t(g.NB) * sizeof(int), s>>>(
       g, static_cast<const uint4*>(qb), static_cast<const char*>(kb),
       static_cast<const char*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
   return hipGetLastError();
