@@ -28,9 +28,9 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from gen.workloads import make_inputs, workload  # noqa: E402
+from gen.workloads import SWEEP_CANDIDATES, SWEEP_SPARSITIES, make_inputs, workload  # noqa: E402
 from paper_2608_03335_amd import spade as S  # noqa: E402
-from paper_2608_03335_amd.pipeline import SpadePath, block_valid_counts  # noqa: E402
+from paper_2608_03335_amd.pipeline import SpadePath, SweepPath, block_valid_counts  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
@@ -45,14 +45,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def kept_flops(p: SpadePath, nvalid: torch.Tensor) -> float:
+def kept_flops_lists(counts, indices, nvalid: torch.Tensor, d: int) -> float:
     """Sum over kept (i, j) of 4 * n_i * n_j * d (matmul FLOPs of the kept work)."""
-    g = p.g
-    NB = g.NB
-    live = torch.arange(NB, device=p.counts.device)[None, None, None, :] < p.counts[..., None].long()
-    idx = p.indices.long().clamp(0, NB - 1)
+    NB = counts.shape[-1]
+    live = torch.arange(NB, device=counts.device)[None, None, None, :] < counts[..., None].long()
+    idx = indices.long().clamp(0, NB - 1)
     nj = torch.where(live, nvalid[idx], torch.zeros_like(idx)).sum(-1)      # [B,H,NB]
-    return float((4.0 * g.d * nvalid[None, None, :].double() * nj.double()).sum().item())
+    return float((4.0 * d * nvalid[None, None, :].double() * nj.double()).sum().item())
+
+
+def kept_flops(p: SpadePath, nvalid: torch.Tensor) -> float:
+    return kept_flops_lists(p.counts, p.indices, nvalid, p.g.d)
 
 
 def stage_bytes(p: SpadePath, nvalid: np.ndarray) -> dict:
@@ -134,6 +137,82 @@ def traffic_record(kernel_file: str, workload_name: str):
     return rec.get("hbm_bytes_per_launch")
 
 
+def sweep(args, dev):
+    """Block-shape sweep on the Hunyuan-Video layer: per-head blocking choice among
+    the candidates, then each head group's Top-K path, at several block sparsities.
+    Prints one JSON line; the selection-side share is (evaluation + per-group
+    blocking/summaries/selection) time over attention time."""
+    cfg = workload("hunyuan_sweep")
+    log("sweep: generating inputs on the GPU")
+    Q, K, V = (x.to(torch.bfloat16) for x in make_inputs(cfg, seed=0, device=dev))
+    stream = torch.cuda.current_stream()
+    rows = []
+    for sp in SWEEP_SPARSITIES:
+        p = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"],
+                      SWEEP_CANDIDATES, sp, device=dev)
+        for _ in range(args.warmup):
+            p.run(Q, K, V)
+        torch.cuda.synchronize()
+        acc = dict(evaluate=0.0, group_select=0.0, attention=0.0, restore=0.0, total=0.0)
+        flops = 0.0
+        for _ in range(args.steps):
+            e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+            t0 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            p.evaluate(Q, K)
+            e[1].record(stream)
+            work = p.work_list(stream)          # host read of the per-head choice
+            marks = []
+            for c, heads in work:
+                m = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                m[0].record(stream)
+                v = p.group_select(c, heads, Q, K, V)
+                m[1].record(stream)
+                p.group_attend(c, v)
+                m[2].record(stream)
+                p.group_restore(c, heads, v)
+                m[3].record(stream)
+                marks.append((c, heads, v, m))
+            t1 = torch.cuda.Event(enable_timing=True)
+            t1.record(stream)
+            torch.cuda.synchronize()
+            acc["evaluate"] += t0.elapsed_time(e[1])
+            acc["total"] += t0.elapsed_time(t1)
+            for c, heads, v, m in marks:
+                acc["group_select"] += m[0].elapsed_time(m[1])
+                acc["attention"] += m[1].elapsed_time(m[2])
+                acc["restore"] += m[2].elapsed_time(m[3])
+        n = max(args.steps, 1)
+        ms = {k: v_ / n for k, v_ in acc.items()}
+        groups = p.groups()
+        for c, heads in p.work_list():
+            v = p.group_views(c, len(heads))
+            nv = torch.from_numpy(block_valid_counts(v["g"])).to(dev)
+            flops += kept_flops_lists(v["counts"], v["indices"], nv, cfg["d"])
+        sel = ms["evaluate"] + ms["group_select"]
+        rows.append({
+            "target_block_sparsity": sp,
+            "topk_per_candidate": dict(zip(["x".join(map(str, c)) for c in SWEEP_CANDIDATES], p.topk)),
+            "heads_per_candidate": {"x".join(map(str, c)): len(hs) for c, hs in zip(SWEEP_CANDIDATES, groups)},
+            "ms_per_call": round(ms["total"], 4),
+            "stage_ms": {k: round(ms[k], 4) for k in ("evaluate", "group_select", "attention", "restore")},
+            "selection_over_attention": round(sel / ms["attention"], 4),
+            "attention_TFLOP/s": round(flops / (ms["attention"] * 1e-3) / 1e12, 2),
+            "attention_mfma_frac": round(flops / (ms["attention"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        })
+        log(json.dumps(rows[-1]))
+        del p
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "block-shape sweep: selection-stage time / attention time",
+                      "config": {"workload": "hunyuan-video-720p-61f attention layer (B1 H24 d128, "
+                                             "grid 16x45x80), per-head choice among blocks "
+                                             + ", ".join("x".join(map(str, c)) for c in SWEEP_CANDIDATES)
+                                             + ", top-k"},
+                      "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
+                      "data": "synthetic (seeded smooth-field + noise Q/K/V, per-head anisotropy)",
+                      "sweep": rows, "device": torch.cuda.get_device_name(0)}))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +222,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true", help="skip the full-mask baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle attention in the CPU baseline (0 = skip)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="run the block-shape sweep (per-head blocking choice) instead")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -162,6 +243,9 @@ def main():
             b.copy_(a)
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes": 1 << 30, "launches": 3}))
+        return
+    if args.sweep:
+        sweep(args, dev)
         return
 
     cfg = workload(args.workload)

@@ -35,7 +35,20 @@ WORKLOADS = {
                    mode="topp", topk=None, tau=0.9, gain=None, freqs=None,
                    split_heads=dict(local=(2.9, 0.03), wide=(2.5, 0.08)),
                    aniso=(1.0, 1.0, 1.0), in_dtype="bf16"),
+    # Hunyuan-Video shape for the block-shape sweep: heads cycle through fields
+    # that vary fastest along t, y, x or evenly, so different candidates win.
+    "hunyuan_sweep": dict(B=1, H=24, d=128, T=16, Hs=45, Ws=80, bt=4, bh=5, bw=8,
+                          mode="topk", topk=None, tau=None, gain=None, g_lo=2.15, g_hi=3.3,
+                          freqs=None, f_cycle=(0.015, 0.03, 0.06),
+                          aniso_cycle=((2.5, 1.0, 1.0), (1.0, 2.5, 1.0), (1.0, 1.0, 2.5),
+                                       (1.0, 1.0, 1.0)),
+                          in_dtype="bf16"),
 }
+
+# Blocking-scheme candidates of the block-shape sweep (two of 128 tokens, two
+# of 160) and its target block sparsities.
+SWEEP_CANDIDATES = ((2, 8, 8), (4, 4, 8), (4, 5, 8), (8, 5, 4))
+SWEEP_SPARSITIES = (0.70, 0.85, 0.95)
 
 
 def _split(cfg: dict, k: int):
@@ -73,6 +86,9 @@ def workload(name: str, **overrides) -> dict:
     cfg["N"] = cfg["T"] * cfg["Hs"] * cfg["Ws"]
     cfg["head_freqs"] = head_freqs(cfg)
     cfg["head_gains"] = head_gains(cfg)
+    if cfg.get("aniso_cycle") is not None:
+        cyc = cfg["aniso_cycle"]
+        cfg["aniso"] = [tuple(cyc[h % len(cyc)]) for h in range(cfg["H"])]
     return cfg
 
 

@@ -5,14 +5,20 @@
  *
  * The path (paper §3.3, Head-wise Sparse Attention), one call per step:
  *   spade_block_reorder      blocking / layout transform and its inverse
+ *                            (optionally for a group of heads, §3.3 (2))
  *   spade_summarize          Summarizer (block means) + optional SICS (§3.2)
  *   spade_estimate_select    inter-block Estimator + Top-K / Top-P index search
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
+ * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
+ *   spade_aggregation_score  per-head Aggregation Score of one candidate scheme
+ *   spade_choose_scheme      per-head argmax over the candidates
  *
  * Conventions shared by every call
  *   - All tensor pointers are DEVICE pointers, owned by the caller, contiguous,
- *     16-byte aligned. The library never allocates, frees or synchronises, and
- *     keeps no state; calls are reentrant and asynchronous on `stream`.
+ *     16-byte aligned (the one host pointer, a reorder call's head list, is
+ *     read before the call returns). The library never allocates, frees or
+ *     synchronises, and keeps no state; calls are reentrant and asynchronous on
+ *     `stream`.
  *   - Shapes follow the paper's problem statement: B batches, H heads, N tokens
  *     of head dimension d, where the N tokens form a (T, Hs, Ws) latent grid
  *     flattened T-major: token n = (t*Hs + y)*Ws + x (§2.1).
@@ -64,17 +70,28 @@ typedef struct {
 /*
  * Blocking (layout transform) and its inverse — paper §3.3: Q, K, V are
  * rearranged into the blocked layout of the selected scheme for intra-block
- * contiguity, and output blocks are restored to the original layout.
+ * contiguity, and output blocks are restored to the original layout. With a
+ * head list this is §3.3 optimisation (2), head grouping: the heads that share
+ * one blocking scheme are gathered from (scattered back to) the full raster
+ * tensor in the same pass, so each group runs as one [B, n_heads, ...] problem.
  *
- *   inverse == 0: x is raster [B,H,N,d], y is blocked [B,H,NB*BS,d];
- *                 y[.., b*BS+s, :] = x[.., token(b,s), :] for real slots,
+ *   heads, n_heads: HOST array of n_heads distinct head indices in [0, H),
+ *                 1 <= n_heads <= 64, read before the call returns; or
+ *                 heads == NULL with n_heads == 0 for all H heads in order.
+ *                 A non-null list with n_heads == 0 moves nothing. Let
+ *                 n = n_heads (H when heads is NULL) and h_k = heads[k] (k).
+ *   inverse == 0: x is raster [B,H,N,d], y is blocked [B,n,NB*BS,d];
+ *                 y[b, k, p*BS+s, :] = x[b, h_k, token(p,s), :] for real slots,
  *                 0 for padding slots (every element of y is written).
- *   inverse == 1: x is blocked, y is raster; padding slots of x are not read.
+ *   inverse == 1: x is blocked [B,n,NB*BS,d], y is raster [B,H,N,d]; only the
+ *                 rows of the listed heads are written; padding slots of x are
+ *                 not read.
  *   dtype: SPADE_BF16 (2-byte elements) or SPADE_FP32 (4-byte). Bit-exact copy.
  *   x and y must not overlap.
  */
 spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y,
-                                 int32_t dtype, int32_t inverse, hipStream_t stream);
+                                 int32_t dtype, int32_t inverse, const int32_t* heads,
+                                 int32_t n_heads, hipStream_t stream);
 
 /*
  * Summarizer and intra-block estimator — paper §3.1 (Summarizer = mean,
@@ -90,6 +107,38 @@ spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y,
 spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb,
                              double* qbar, double* kbar, double* sics_q, double* sics_k,
                              hipStream_t stream);
+
+/*
+ * Aggregation Score of one blocking-scheme candidate — paper §3.2, Eq. (3):
+ * a head's AS under a scheme is the sum over its blocks of SICS, for Q and for K.
+ *
+ *   sics_q, sics_k: fp64 [B,H,NB], as written by spade_summarize under g's scheme.
+ *   as_q, as_k:   out, nullable, fp64 [B,H]: sum_p SICS_p / sum_p n_p^2, where n_p
+ *                 is block p's real-token count. The divisor is the score of a
+ *                 block whose vectors are all parallel, so candidates with
+ *                 different block sizes or padding compare on one scale (for
+ *                 equal unpadded blocks it is a constant factor). The raw Eq. (3)
+ *                 sum is as_q * sum_p n_p^2.
+ *   as_qk:        out, fp64 [B,H]: as_q + as_k, the score spade_choose_scheme ranks.
+ *   Each output is a fixed-order reduction (deterministic).
+ */
+spade_status spade_aggregation_score(const spade_geom* g, const double* sics_q,
+                                     const double* sics_k, double* as_q, double* as_k,
+                                     double* as_qk, hipStream_t stream);
+
+/*
+ * Selected Blocking Scheme per head — paper §3.2: each head takes the candidate
+ * with the highest Aggregation Score.
+ *
+ *   as_qk:  fp64 [C,B,H]: row c is spade_aggregation_score's as_qk for candidate c.
+ *   choice: out, int32 [H]: per head, the candidate c with the largest batch mean
+ *           (1/B) sum_b as_qk[c,b,h]; ties go to the lower c (a NaN never wins
+ *           over candidate 0's value).
+ *   best:   out, nullable, fp64 [H]: that mean (the Selected Aggregation Score).
+ *   1 <= C <= 1024. B or H equal to 0 is a no-op.
+ */
+spade_status spade_choose_scheme(const double* as_qk, int32_t C, int32_t B, int32_t H,
+                                 int32_t* choice, double* best, hipStream_t stream);
 
 /*
  * Inter-block Estimator + Top-K / Top-P index search — paper §3.3 (inter-block

@@ -33,7 +33,12 @@ design notes):
   * rows are ranked by (score descending, block index ascending);
   * Top-P keeps the shortest prefix of that ranking whose softmax mass over the
     row's block scores reaches tau (at least one block); tau >= 1 keeps all;
-  * kept indices are reported in ascending block order.
+  * kept indices are reported in ascending block order;
+  * a candidate blocking is scored by AS(Q) + AS(K), each normalised by
+    sum_b n_b^2 so that block sizes and padding compare; a head's score is its
+    batch mean; the first candidate with the highest score wins;
+  * the block-shape sweep keeps k = max(1, round((1 - s) NB)) blocks per row
+    for a target block sparsity s.
 
 Every array here is float64 (inputs are upcast first). Shapes: Q, K, V are
 [B, H, N, d]; blocked tensors are [B, H, NB*BS, d].
@@ -218,6 +223,76 @@ def aggregation_score(sics: np.ndarray, g: Geometry):
     _, n_valid = block_tables(g)
     raw = sics.sum(axis=-1)
     return raw, raw / float((n_valid.astype(np.float64) ** 2).sum())
+
+
+def scheme_scores(Q, K, g: Geometry) -> np.ndarray:
+    """Per-(batch, head) score of one candidate blocking: AS_norm(Q) + AS_norm(K).
+
+    §3.2 builds the candidates' scores from Q and K blocked under each scheme;
+    Eq. (3) defines AS for Q as the sum of block SICS, and K is treated alike.
+    """
+    Q, K = np.asarray(Q, np.float64), np.asarray(K, np.float64)
+    _, as_q = aggregation_score(block_sics(reorder(Q, g), g), g)
+    _, as_k = aggregation_score(block_sics(reorder(K, g), g), g)
+    return as_q + as_k
+
+
+def choose_schemes(as_qk: np.ndarray):
+    """Selected Blocking Scheme per head (§3.2): highest AS wins.
+
+    as_qk: [C, B, H] candidate scores. A head's score for candidate c is its mean
+    over the batch, so one scheme serves the head in every batch element; ties go
+    to the lower candidate index. Returns (choice [H] int, best [H]).
+    """
+    per_head = np.asarray(as_qk, np.float64).mean(axis=1)        # [C, H]
+    choice = np.zeros(per_head.shape[1], dtype=np.int64)
+    best = per_head[0].copy()
+    for c in range(1, per_head.shape[0]):                        # first maximum wins
+        better = per_head[c] > best
+        choice[better], best[better] = c, per_head[c][better]
+    return choice, best
+
+
+def head_groups(choice: np.ndarray, C: int):
+    """Head grouping (§3.3 (2)): ascending head list per candidate (may be empty)."""
+    return [[int(h) for h in np.flatnonzero(np.asarray(choice) == c)] for c in range(C)]
+
+
+def sweep_topk(sparsity: float, NB: int) -> int:
+    """Blocks kept per query row for a target block sparsity s: max(1, round((1-s) NB))."""
+    return max(1, int(np.floor((1.0 - sparsity) * NB + 0.5)))
+
+
+def spade_sweep_attention(Q, K, V, grid, block_shapes, sparsity: float, scale=None):
+    """Head-wise blocking choice among candidates, then each head group's path.
+
+    For every candidate (bt, bh, bw): blocking of Q and K, SICS, normalised AS
+    (Eq. (3)); each head takes its best candidate (§3.2); heads sharing a scheme
+    form a group (§3.3 (2)) that runs blocking -> means -> scores -> Top-K with
+    k = sweep_topk(sparsity, NB) -> Eq. (2) -> restore, into the full output.
+    grid = (T, Hs, Ws). Returns dict(O, choice, best, as_qk, groups, per-group
+    counts/indices).
+    """
+    Q, K, V = (np.asarray(a, dtype=np.float64) for a in (Q, K, V))
+    d = Q.shape[-1]
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    geoms = [Geometry(*grid, *bs) for bs in block_shapes]
+    as_qk = np.stack([scheme_scores(Q, K, g) for g in geoms])     # [C, B, H]
+    choice, best = choose_schemes(as_qk)
+    groups = head_groups(choice, len(geoms))
+    O = np.zeros_like(Q)
+    per_group = []
+    for c, heads in enumerate(groups):
+        if not heads:
+            per_group.append(None)
+            continue
+        g = geoms[c]
+        r = spade_attention(Q[:, heads], K[:, heads], V[:, heads], g, "topk",
+                            topk=sweep_topk(sparsity, g.NB), scale=scale)
+        O[:, heads] = r["O"]
+        per_group.append(dict(heads=heads, counts=r["counts"], indices=r["indices"],
+                              topk=sweep_topk(sparsity, g.NB)))
+    return dict(O=O, choice=choice, best=best, as_qk=as_qk, groups=groups, per_group=per_group)
 
 
 # --------------------------------------------------------------------------

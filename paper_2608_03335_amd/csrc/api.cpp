@@ -82,7 +82,8 @@ const char* spade_status_string(spade_status s) {
 const char* spade_last_error(void) { return g_last_error; }
 
 spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y, int32_t dtype,
-                                 int32_t inverse, hipStream_t stream) {
+                                 int32_t inverse, const int32_t* heads, int32_t n_heads,
+                                 hipStream_t stream) {
   spade::DevGeom dg;
   bool empty = false;
   spade_status st = check_geom(g, &dg, &empty);
@@ -91,13 +92,34 @@ spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y, in
     return fail(SPADE_ERR_INVALID_ARG, "dtype must be SPADE_BF16 or SPADE_FP32 (got %d)", dtype);
   if (inverse != 0 && inverse != 1)
     return fail(SPADE_ERR_INVALID_ARG, "inverse must be 0 or 1 (got %d)", inverse);
-  if (empty) return SPADE_OK;
+  spade::HeadMap hm;
+  hm.n = dg.H;
+  hm.ident = 1;
+  if (heads == nullptr) {
+    if (n_heads != 0)
+      return fail(SPADE_ERR_INVALID_ARG, "n_heads must be 0 when heads is null (got %d)", n_heads);
+  } else {
+    if (n_heads < 0 || n_heads > spade::kMaxHeadList)
+      return fail(SPADE_ERR_INVALID_ARG, "n_heads must lie in [0, %d] (got %d)",
+                  spade::kMaxHeadList, n_heads);
+    hm.n = n_heads;
+    hm.ident = 0;
+    for (int k = 0; k < n_heads; ++k) {
+      if (heads[k] < 0 || heads[k] >= dg.H)
+        return fail(SPADE_ERR_INVALID_ARG, "heads[%d]=%d outside [0, H=%d)", k, heads[k], dg.H);
+      for (int j = 0; j < k; ++j)
+        if (heads[j] == heads[k])
+          return fail(SPADE_ERR_INVALID_ARG, "head %d listed twice", heads[k]);
+      hm.h[k] = heads[k];
+    }
+  }
+  if (empty || hm.n == 0) return SPADE_OK;
   if (!x || !y) return fail(SPADE_ERR_INVALID_ARG, "x and y must be non-null");
   if (!aligned16(x) || !aligned16(y))
     return fail(SPADE_ERR_INVALID_ARG, "x and y must be 16-byte aligned");
   if (x == y) return fail(SPADE_ERR_INVALID_ARG, "x and y must not alias");
   const int esize = dtype == SPADE_BF16 ? 2 : 4;
-  return hip_status(spade::launch_reorder(dg, x, y, esize, inverse, stream), "reorder launch");
+  return hip_status(spade::launch_reorder(dg, x, y, esize, inverse, hm, stream), "reorder launch");
 }
 
 spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb, double* qbar,
@@ -115,6 +137,34 @@ spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb
     return fail(SPADE_ERR_INVALID_ARG, "qb, kb, qbar and kbar must be 16-byte aligned");
   return hip_status(spade::launch_summarize(dg, qb, kb, qbar, kbar, sics_q, sics_k, stream),
                     "summarize launch");
+}
+
+spade_status spade_aggregation_score(const spade_geom* g, const double* sics_q,
+                                     const double* sics_k, double* as_q, double* as_k,
+                                     double* as_qk, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (empty) return SPADE_OK;
+  if (!sics_q || !sics_k || !as_qk)
+    return fail(SPADE_ERR_INVALID_ARG, "sics_q, sics_k and as_qk must be non-null");
+  return hip_status(spade::launch_aggregation_score(dg, sics_q, sics_k, as_q, as_k, as_qk, stream),
+                    "aggregation_score launch");
+}
+
+spade_status spade_choose_scheme(const double* as_qk, int32_t C, int32_t B, int32_t H,
+                                 int32_t* choice, double* best, hipStream_t stream) {
+  if (C < 1 || C > spade::kMaxCandidates)
+    return fail(SPADE_ERR_INVALID_ARG, "candidate count C must lie in [1, %d] (got %d)",
+                spade::kMaxCandidates, C);
+  if (B < 0 || H < 0) return fail(SPADE_ERR_INVALID_ARG, "negative B or H (B=%d H=%d)", B, H);
+  if (int64_t(C) * B * H > (int64_t(1) << 40) || H > (1 << 24))
+    return fail(SPADE_ERR_UNSUPPORTED, "score table too large (C=%d B=%d H=%d)", C, B, H);
+  if (B == 0 || H == 0) return SPADE_OK;
+  if (!as_qk || !choice) return fail(SPADE_ERR_INVALID_ARG, "as_qk and choice must be non-null");
+  return hip_status(spade::launch_choose_scheme(as_qk, C, B, H, choice, best, stream),
+                    "choose_scheme launch");
 }
 
 spade_status spade_estimate_select(const spade_geom* g, const double* qbar, const double* kbar,

@@ -24,16 +24,27 @@ __device__ __forceinline__ int64_t slot_token(const DevGeom& g, const BlockExt& 
   return (int64_t(e.t0 + dt) * g.Hs + (e.y0 + dy)) * g.Ws + (e.x0 + dx);
 }
 
-// raster [BH, N, row] -> blocked [BH, NB*BS, row]; padding slots get zeros.
+// grid.y enumerates (batch, listed head): blocked-side index, raster-side index
+__device__ __forceinline__ void head_pair(const DevGeom& g, const HeadMap& hm, int64_t* blocked,
+                                          int64_t* raster) {
+  const int by = blockIdx.y;
+  const int b = by / hm.n, k = by - b * hm.n;
+  *blocked = by;
+  *raster = int64_t(b) * g.H + (hm.ident ? k : hm.h[k]);
+}
+
+// raster [B, H, N, row] -> blocked [B, n, NB*BS, row]; padding slots get zeros.
 template <int VPR>
-__global__ void __launch_bounds__(kThreads) reorder_fwd(DevGeom g, const uint4* __restrict__ x,
+__global__ void __launch_bounds__(kThreads) reorder_fwd(DevGeom g, HeadMap hm,
+                                                        const uint4* __restrict__ x,
                                                         uint4* __restrict__ y) {
   const int b = blockIdx.x;
-  const int64_t bh = blockIdx.y;
+  int64_t bh_blk, bh_ras;
+  head_pair(g, hm, &bh_blk, &bh_ras);
   const BlockExt e = block_ext(g, b);
   const float r_ew = 1.0f / float(e.ew), r_eh = 1.0f / float(e.eh);
-  const uint4* src = x + bh * g.N * VPR;
-  uint4* dst = y + (bh * g.NB + b) * int64_t(g.BS) * VPR;
+  const uint4* src = x + bh_ras * g.N * VPR;
+  uint4* dst = y + (bh_blk * g.NB + b) * int64_t(g.BS) * VPR;
   const int total = g.BS * VPR;
   const int valid = e.n * VPR;
   for (int f0 = threadIdx.x; f0 < total; f0 += kThreads * kUnroll) {
@@ -55,16 +66,19 @@ __global__ void __launch_bounds__(kThreads) reorder_fwd(DevGeom g, const uint4* 
   }
 }
 
-// blocked [BH, NB*BS, row] -> raster [BH, N, row]; padding slots are not read.
+// blocked [B, n, NB*BS, row] -> raster [B, H, N, row] (listed heads only);
+// padding slots are not read.
 template <int VPR>
-__global__ void __launch_bounds__(kThreads) reorder_inv(DevGeom g, const uint4* __restrict__ xb,
+__global__ void __launch_bounds__(kThreads) reorder_inv(DevGeom g, HeadMap hm,
+                                                        const uint4* __restrict__ xb,
                                                         uint4* __restrict__ y) {
   const int b = blockIdx.x;
-  const int64_t bh = blockIdx.y;
+  int64_t bh_blk, bh_ras;
+  head_pair(g, hm, &bh_blk, &bh_ras);
   const BlockExt e = block_ext(g, b);
   const float r_ew = 1.0f / float(e.ew), r_eh = 1.0f / float(e.eh);
-  const uint4* src = xb + (bh * g.NB + b) * int64_t(g.BS) * VPR;
-  uint4* dst = y + bh * g.N * VPR;
+  const uint4* src = xb + (bh_blk * g.NB + b) * int64_t(g.BS) * VPR;
+  uint4* dst = y + bh_ras * g.N * VPR;
   const int valid = e.n * VPR;
   for (int f0 = threadIdx.x; f0 < valid; f0 += kThreads * kUnroll) {
     uint4 v[kUnroll];
@@ -85,13 +99,14 @@ __global__ void __launch_bounds__(kThreads) reorder_inv(DevGeom g, const uint4* 
 }
 
 template <int VPR>
-hipError_t launch_vpr(const DevGeom& g, const void* x, void* y, int inverse, hipStream_t s) {
-  const dim3 grid(g.NB, g.B * g.H);
+hipError_t launch_vpr(const DevGeom& g, const void* x, void* y, int inverse, const HeadMap& hm,
+                      hipStream_t s) {
+  const dim3 grid(g.NB, g.B * hm.n);
   if (inverse)
-    reorder_inv<VPR><<<grid, kThreads, 0, s>>>(g, static_cast<const uint4*>(x),
+    reorder_inv<VPR><<<grid, kThreads, 0, s>>>(g, hm, static_cast<const uint4*>(x),
                                                static_cast<uint4*>(y));
   else
-    reorder_fwd<VPR><<<grid, kThreads, 0, s>>>(g, static_cast<const uint4*>(x),
+    reorder_fwd<VPR><<<grid, kThreads, 0, s>>>(g, hm, static_cast<const uint4*>(x),
                                                static_cast<uint4*>(y));
   return hipGetLastError();
 }
@@ -99,11 +114,11 @@ hipError_t launch_vpr(const DevGeom& g, const void* x, void* y, int inverse, hip
 }  // namespace
 
 hipError_t launch_reorder(const DevGeom& g, const void* x, void* y, int esize, int inverse,
-                          hipStream_t s) {
+                          const HeadMap& hm, hipStream_t s) {
   switch (g.d * esize / 16) {
-    case 8: return launch_vpr<8>(g, x, y, inverse, s);
-    case 16: return launch_vpr<16>(g, x, y, inverse, s);
-    case 32: return launch_vpr<32>(g, x, y, inverse, s);
+    case 8: return launch_vpr<8>(g, x, y, inverse, hm, s);
+    case 16: return launch_vpr<16>(g, x, y, inverse, hm, s);
+    case 32: return launch_vpr<32>(g, x, y, inverse, hm, s);
   }
   return hipErrorInvalidValue;
 }

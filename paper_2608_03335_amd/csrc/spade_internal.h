@@ -39,9 +39,22 @@ __device__ __forceinline__ BlockExt block_ext(const DevGeom& g, int b) {
   return e;
 }
 
+constexpr int kMaxHeadList = 64;  // head subset of one reorder call (passed by value)
+
+// Which heads a reorder call moves: blocked-side head k <-> raster-side head h[k].
+// ident = 1 means all H heads in order (h[] unused).
+struct HeadMap {
+  int n, ident;
+  int h[kMaxHeadList];
+};
+
 // Launchers (each returns hipGetLastError() after its launches).
 hipError_t launch_reorder(const DevGeom& g, const void* x, void* y, int esize, int inverse,
-                          hipStream_t s);
+                          const HeadMap& heads, hipStream_t s);
+hipError_t launch_aggregation_score(const DevGeom& g, const double* sics_q, const double* sics_k,
+                                    double* as_q, double* as_k, double* as_sum, hipStream_t s);
+hipError_t launch_choose_scheme(const double* as_qk, int C, int B, int H, int* choice,
+                                double* best, hipStream_t s);
 hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
                             double* kbar, double* sics_q, double* sics_k, hipStream_t s);
 hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const double* kbar,
@@ -56,5 +69,6 @@ hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void
 constexpr int kMaxBS = 256;        // attention: one wave per 32 query rows, <= 8 waves
 constexpr int kMaxSelectNB = 1024;  // selection: one row of scores per wave in registers
 constexpr int kMaxAttnNB = 16384;   // attention: a work item's kept list is staged in LDS
+constexpr int kMaxCandidates = 1024;  // blocking-scheme candidates of one choose call
 
 }  // namespace spade

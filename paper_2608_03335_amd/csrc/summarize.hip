@@ -116,7 +116,78 @@ hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, double* qb
   return hipGetLastError();
 }
 
+// Per head: the batch mean of every candidate's aggregation score, then the
+// first candidate with the largest mean (ties go to the lower candidate index).
+__global__ void __launch_bounds__(kThreads) choose_scheme_kernel(const double* __restrict__ as_qk,
+                                                                 int C, int B, int H,
+                                                                 int* __restrict__ choice,
+                                                                 double* __restrict__ best) {
+  const int h = blockIdx.x * kThreads + threadIdx.x;
+  if (h >= H) return;
+  int arg = 0;
+  double top = 0.0;
+  for (int c = 0; c < C; ++c) {
+    double s = 0.0;
+    for (int b = 0; b < B; ++b) s += as_qk[(int64_t(c) * B + b) * H + h];
+    s /= double(B);
+    if (c == 0 || s > top) {
+      top = s;
+      arg = c;
+    }
+  }
+  choice[h] = arg;
+  if (best) best[h] = top;
+}
+
 }  // namespace
+
+hipError_t launch_choose_scheme(const double* as_qk, int C, int B, int H, int* choice,
+                                double* best, hipStream_t s) {
+  choose_scheme_kernel<<<dim3((H + kThreads - 1) / kThreads), kThreads, 0, s>>>(as_qk, C, B, H,
+                                                                               choice, best);
+  return hipGetLastError();
+}
+
+// Aggregation Score, Eq. (3): per head, the sum of its blocks' SICS, divided by
+// sum_b n_b^2 (the value when every block's vectors are parallel) so that
+// blockings with different block sizes or padding compare on one scale.
+// One workgroup per head; each thread adds a fixed stride of blocks, then a
+// fixed-shape tree, so the result does not depend on scheduling.
+__global__ void __launch_bounds__(kThreads) aggregation_score_kernel(
+    DevGeom g, const double* __restrict__ sics_q, const double* __restrict__ sics_k,
+    double* __restrict__ as_q, double* __restrict__ as_k, double* __restrict__ as_sum) {
+  __shared__ double red[3][kThreads];
+  const int64_t bh = blockIdx.x;
+  double sq = 0.0, sk = 0.0, norm = 0.0;
+  for (int b = threadIdx.x; b < g.NB; b += kThreads) {
+    const double n = double(block_ext(g, b).n);
+    sq += sics_q[bh * g.NB + b];
+    sk += sics_k[bh * g.NB + b];
+    norm += n * n;
+  }
+  red[0][threadIdx.x] = sq;
+  red[1][threadIdx.x] = sk;
+  red[2][threadIdx.x] = norm;
+  __syncthreads();
+  for (int off = kThreads / 2; off > 0; off >>= 1) {
+    if (threadIdx.x < off)
+      for (int c = 0; c < 3; ++c) red[c][threadIdx.x] += red[c][threadIdx.x + off];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double q = red[0][0] / red[2][0], k = red[1][0] / red[2][0];
+    if (as_q) as_q[bh] = q;
+    if (as_k) as_k[bh] = k;
+    as_sum[bh] = q + k;
+  }
+}
+
+hipError_t launch_aggregation_score(const DevGeom& g, const double* sics_q, const double* sics_k,
+                                    double* as_q, double* as_k, double* as_sum, hipStream_t s) {
+  aggregation_score_kernel<<<dim3(g.B * g.H), kThreads, 0, s>>>(g, sics_q, sics_k, as_q, as_k,
+                                                                 as_sum);
+  return hipGetLastError();
+}
 
 hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
                             double* kbar, double* sics_q, double* sics_k, hipStream_t s) {

@@ -78,3 +78,121 @@ class SpadePath:
         self.attend(stream=stream)
         self.restore(stream)
         return self.O
+
+
+def _chunks(heads, n):
+    return [heads[i:i + n] for i in range(0, len(heads), n)]
+
+
+class SweepPath:
+    """Head-wise blocking choice over candidate schemes, then one path per head group.
+
+    Evaluation (§3.2): for every candidate, blocking of Q and K for all heads,
+    summaries with SICS, the normalised Aggregation Score, then the per-head
+    argmax on the device. The choice is read back to the host (the one sync) to
+    form the head groups; each group then runs blocking with its head list
+    (§3.3 (2)), summaries, Top-K selection with k = max(1, round((1 - s) NB)),
+    block-sparse attention and the inverse blocking into the full output.
+    """
+
+    def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda"):
+        self.B, self.H, self.d = B, H, d
+        self.shapes = [tuple(c) for c in candidates]
+        self.sparsity = float(sparsity)
+        self.scale = float(scale if scale is not None else 1.0 / math.sqrt(d))
+        self.geoms = [S.geom(B, H, d, T, Hs, Ws, *c) for c in self.shapes]
+        bf, f64, dev = torch.bfloat16, torch.float64, device
+        self.topk = [max(1, int(math.floor((1.0 - self.sparsity) * g.NB + 0.5))) for g in self.geoms]
+        # evaluation buffers, one set per candidate (all heads)
+        self.ev = []
+        for g in self.geoms:
+            rows = g.NB * g.BS
+            self.ev.append(dict(
+                Qb=torch.empty((B, H, rows, d), dtype=bf, device=dev),
+                Kb=torch.empty((B, H, rows, d), dtype=bf, device=dev),
+                qbar=torch.empty((B, H, g.NB, d), dtype=f64, device=dev),
+                kbar=torch.empty((B, H, g.NB, d), dtype=f64, device=dev),
+                sics_q=torch.empty((B, H, g.NB), dtype=f64, device=dev),
+                sics_k=torch.empty((B, H, g.NB), dtype=f64, device=dev)))
+        C = len(self.geoms)
+        self.as_qk = torch.empty((C, B, H), dtype=f64, device=dev)
+        self.choice = torch.empty(H, dtype=torch.int32, device=dev)
+        self.best = torch.empty(H, dtype=f64, device=dev)
+        # group buffers: flat storage for up to min(H, 64) heads per candidate,
+        # viewed as a contiguous [B, n, ...] tensor for a group of n heads
+        cap = min(H, S.MAX_HEAD_LIST)
+        self.gb = []
+        for g in self.geoms:
+            rows = g.NB * g.BS
+            self.gb.append(dict(
+                Q=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
+                K=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
+                V=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
+                O=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
+                qbar=torch.empty(B * cap * g.NB * d, dtype=f64, device=dev),
+                kbar=torch.empty(B * cap * g.NB * d, dtype=f64, device=dev),
+                counts=torch.empty(B * cap * g.NB, dtype=torch.int32, device=dev),
+                indices=torch.empty(B * cap * g.NB * g.NB, dtype=torch.int32, device=dev)))
+        self.ws = torch.empty(max(max(S.spade_attn_workspace_bytes(g) for g in self.geoms), 1),
+                              dtype=torch.uint8, device=dev)
+        self.O = torch.empty((B, H, T * Hs * Ws, d), dtype=bf, device=dev)
+
+    def evaluate(self, Q, K, stream=None):
+        for c, (g, e) in enumerate(zip(self.geoms, self.ev)):
+            S.spade_block_reorder(g, Q, e["Qb"], stream=stream)
+            S.spade_block_reorder(g, K, e["Kb"], stream=stream)
+            S.spade_summarize(g, e["Qb"], e["Kb"], e["qbar"], e["kbar"], e["sics_q"], e["sics_k"],
+                              stream=stream)
+            S.spade_aggregation_score(g, e["sics_q"], e["sics_k"], self.as_qk[c], stream=stream)
+        S.spade_choose_scheme(self.as_qk, self.choice, self.best, stream=stream)
+
+    def groups(self, stream=None):
+        """Host copy of the choice (waits for `stream`) -> ascending head list per candidate."""
+        if stream is not None:
+            stream.synchronize()
+        ch = self.choice.cpu().tolist()
+        return [[h for h in range(self.H) if ch[h] == c] for c in range(len(self.geoms))]
+
+    def group_views(self, c, n):
+        g = self.geoms[c]
+        gg = S.geom(self.B, n, self.d, g.T, g.Hs, g.Ws, g.bt, g.bh, g.bw)
+        b, rows, NB = self.gb[c], g.NB * g.BS, g.NB
+        v = dict(g=gg)
+        for k in ("Q", "K", "V", "O"):
+            v[k] = b[k][: self.B * n * rows * self.d].view(self.B, n, rows, self.d)
+        for k in ("qbar", "kbar"):
+            v[k] = b[k][: self.B * n * NB * self.d].view(self.B, n, NB, self.d)
+        v["counts"] = b["counts"][: self.B * n * NB].view(self.B, n, NB)
+        v["indices"] = b["indices"][: self.B * n * NB * NB].view(self.B, n, NB, NB)
+        return v
+
+    # group stages, separately callable so they can be timed
+    def group_select(self, c, heads, Q, K, V, stream=None):
+        g, v = self.geoms[c], self.group_views(c, len(heads))
+        for x, key in ((Q, "Q"), (K, "K"), (V, "V")):
+            S.spade_block_reorder(g, x, v[key], heads=heads, stream=stream)
+        S.spade_summarize(v["g"], v["Q"], v["K"], v["qbar"], v["kbar"], stream=stream)
+        S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
+                                self.scale, v["counts"], v["indices"], stream=stream)
+        return v
+
+    def group_attend(self, c, v, stream=None):
+        S.spade_block_sparse_attn(v["g"], v["Q"], v["K"], v["V"], v["counts"], v["indices"],
+                                  self.scale, v["O"], None, self.ws, stream=stream)
+
+    def group_restore(self, c, heads, v, stream=None):
+        S.spade_block_reorder(self.geoms[c], v["O"], self.O, inverse=True, heads=heads,
+                              stream=stream)
+
+    def work_list(self, stream=None):
+        """[(candidate, heads)] with every group split into chunks of <= 64 heads."""
+        return [(c, hs) for c, grp in enumerate(self.groups(stream))
+                for hs in _chunks(grp, S.MAX_HEAD_LIST)]
+
+    def run(self, Q, K, V, stream=None):
+        self.evaluate(Q, K, stream)
+        for c, heads in self.work_list(stream):
+            v = self.group_select(c, heads, Q, K, V, stream)
+            self.group_attend(c, v, stream)
+            self.group_restore(c, heads, v, stream)
+        return self.O

@@ -18,9 +18,10 @@ SPADE_OK, SPADE_ERR_INVALID_ARG, SPADE_ERR_UNSUPPORTED, SPADE_ERR_WORKSPACE, SPA
 SPADE_BF16, SPADE_FP32 = 0, 1
 SPADE_TOPK, SPADE_TOPP = 0, 1
 
-EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_estimate_select",
-            "spade_attn_workspace_bytes", "spade_block_sparse_attn",
-            "spade_status_string", "spade_last_error")
+EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_aggregation_score",
+            "spade_choose_scheme", "spade_estimate_select", "spade_attn_workspace_bytes",
+            "spade_block_sparse_attn", "spade_status_string", "spade_last_error")
+MAX_HEAD_LIST = 64
 
 
 class SpadeError(RuntimeError):
@@ -63,8 +64,10 @@ def lib() -> ctypes.CDLL:
         vp, i32, f64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_double, ctypes.c_size_t
         G = ctypes.POINTER(spade_geom)
         sig = {
-            "spade_block_reorder": (i32, [G, vp, vp, i32, i32, vp]),
+            "spade_block_reorder": (i32, [G, vp, vp, i32, i32, ctypes.POINTER(i32), i32, vp]),
             "spade_summarize": (i32, [G, vp, vp, vp, vp, vp, vp, vp]),
+            "spade_aggregation_score": (i32, [G, vp, vp, vp, vp, vp, vp]),
+            "spade_choose_scheme": (i32, [vp, i32, i32, i32, vp, vp, vp]),
             "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
@@ -95,14 +98,37 @@ def _check(status: int):
                                  f"{L.spade_last_error().decode()}")
 
 
-def spade_block_reorder(g: spade_geom, x, y, inverse: bool = False, stream=None):
+def _head_list(heads):
+    if heads is None:
+        return None, 0
+    hs = [int(h) for h in heads]
+    return (ctypes.c_int32 * max(len(hs), 1))(*hs), len(hs)
+
+
+def spade_block_reorder(g: spade_geom, x, y, inverse: bool = False, heads=None, stream=None):
+    """heads: None (all heads) or a sequence of head indices (the group's heads)."""
     dtype = SPADE_BF16 if x.dtype == torch.bfloat16 else SPADE_FP32
-    _check(lib().spade_block_reorder(ctypes.byref(g), _p(x), _p(y), dtype, int(inverse), _s(stream)))
+    arr, n = _head_list(heads)
+    _check(lib().spade_block_reorder(ctypes.byref(g), _p(x), _p(y), dtype, int(inverse), arr, n,
+                                     _s(stream)))
 
 
 def spade_summarize(g: spade_geom, qb, kb, qbar, kbar, sics_q=None, sics_k=None, stream=None):
     _check(lib().spade_summarize(ctypes.byref(g), _p(qb), _p(kb), _p(qbar), _p(kbar),
                                  _p(sics_q), _p(sics_k), _s(stream)))
+
+
+def spade_aggregation_score(g: spade_geom, sics_q, sics_k, as_qk, as_q=None, as_k=None,
+                            stream=None):
+    _check(lib().spade_aggregation_score(ctypes.byref(g), _p(sics_q), _p(sics_k), _p(as_q),
+                                         _p(as_k), _p(as_qk), _s(stream)))
+
+
+def spade_choose_scheme(as_qk, choice, best=None, stream=None):
+    """as_qk: fp64 [C, B, H] device tensor; choice: int32 [H]; best: fp64 [H] or None."""
+    C, B, H = as_qk.shape
+    _check(lib().spade_choose_scheme(_p(as_qk), int(C), int(B), int(H), _p(choice), _p(best),
+                                     _s(stream)))
 
 
 def spade_estimate_select(g: spade_geom, qbar, kbar, mode: int, topk: int, tau: float,

@@ -21,10 +21,10 @@ def _declared():
     return sorted(set(re.findall(r"\b(spade_[a-z_]+)\s*\(", text)))
 
 
-def test_header_declares_the_four_path_calls():
+def test_header_declares_the_path_calls():
     names = _declared()
     for n in ("spade_block_reorder", "spade_summarize", "spade_estimate_select",
-              "spade_block_sparse_attn"):
+              "spade_block_sparse_attn", "spade_aggregation_score", "spade_choose_scheme"):
         assert n in names
 
 
@@ -68,27 +68,66 @@ def test_status_strings():
 def test_geometry_validation(kw, expect):
     L = S.lib()
     g = _g(**kw)
-    st, msg = _status(L.spade_block_reorder, ctypes.byref(g), FAKE, FAKE, 0, 0, None)
+    st, msg = _status(L.spade_block_reorder, ctypes.byref(g), FAKE, FAKE, 0, 0, None, 0, None)
     assert st == expect and msg
 
 
 def test_reorder_argument_errors():
     L = S.lib()
     g = _g()
-    assert L.spade_block_reorder(None, FAKE, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
-    assert L.spade_block_reorder(ctypes.byref(g), NULL, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
-    assert L.spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None) == S.SPADE_ERR_INVALID_ARG  # alias
-    assert L.spade_block_reorder(ctypes.byref(g), FAKE, MISALIGNED, 0, 0, None) == S.SPADE_ERR_INVALID_ARG
-    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 7, 0, None) == S.SPADE_ERR_INVALID_ARG
-    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 0, 2, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(None, FAKE, FAKE, 0, 0, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), NULL, FAKE, 0, 0, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None, 0, None) == S.SPADE_ERR_INVALID_ARG  # alias
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, MISALIGNED, 0, 0, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 7, 0, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 0, 2, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+
+
+def _heads(*hs):
+    return (ctypes.c_int32 * max(len(hs), 1))(*hs)
+
+
+@pytest.mark.parametrize("heads,n,expect", [
+    (None, 1, S.SPADE_ERR_INVALID_ARG),            # null list needs n_heads == 0
+    ((0, 2), 2, S.SPADE_ERR_INVALID_ARG),           # head 2 outside [0, H=2)
+    ((1, -1), 2, S.SPADE_ERR_INVALID_ARG),          # negative head
+    ((1, 1), 2, S.SPADE_ERR_INVALID_ARG),           # duplicate
+    ((0,), -1, S.SPADE_ERR_INVALID_ARG),            # negative count
+    (tuple(range(65)), 65, S.SPADE_ERR_INVALID_ARG),  # more than 64 heads
+    ((1,), 0, S.SPADE_OK),                          # empty list: nothing to move
+])
+def test_reorder_head_list_errors(heads, n, expect):
+    L = S.lib()
+    g = _g(H=2) if n != 65 else _g(H=100)
+    arr = None if heads is None else _heads(*heads)
+    for inverse in (0, 1):
+        st = L.spade_block_reorder(ctypes.byref(g), FAKE, ctypes.c_void_p(0x2000), 0, inverse,
+                                   arr, n, None)
+        assert st == expect, (heads, n, inverse)
+
+
+def test_aggregation_and_choice_errors():
+    L = S.lib()
+    g = _g()
+    assert L.spade_aggregation_score(ctypes.byref(g), FAKE, NULL, NULL, NULL, FAKE, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_aggregation_score(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_aggregation_score(ctypes.byref(_g(d=96)), FAKE, FAKE, NULL, NULL, FAKE, None) == S.SPADE_ERR_UNSUPPORTED
+    assert L.spade_choose_scheme(FAKE, 0, 1, 2, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_choose_scheme(FAKE, 1025, 1, 2, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_choose_scheme(FAKE, 2, -1, 2, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_choose_scheme(NULL, 2, 1, 2, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_choose_scheme(FAKE, 2, 1, 2, NULL, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_choose_scheme(NULL, 2, 0, 2, NULL, NULL, None) == S.SPADE_OK
+    assert L.spade_choose_scheme(NULL, 2, 1, 0, NULL, NULL, None) == S.SPADE_OK
 
 
 def test_empty_problem_is_a_no_op():
     L = S.lib()
     for kw in (dict(B=0), dict(H=0), dict(T=0)):
         g = _g(**kw)
-        assert L.spade_block_reorder(ctypes.byref(g), NULL, NULL, 0, 0, None) == S.SPADE_OK
+        assert L.spade_block_reorder(ctypes.byref(g), NULL, NULL, 0, 0, None, 0, None) == S.SPADE_OK
         assert L.spade_summarize(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, NULL, None) == S.SPADE_OK
+        assert L.spade_aggregation_score(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, None) == S.SPADE_OK
         assert L.spade_estimate_select(ctypes.byref(g), NULL, NULL, 0, 1, 0.0, 1.0, NULL, NULL, NULL, None) == S.SPADE_OK
         assert L.spade_attn_workspace_bytes(ctypes.byref(g)) == 0
         assert L.spade_block_sparse_attn(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, 1.0,
@@ -152,4 +191,4 @@ def test_attention_workspace_and_pointer_errors():
 def test_python_binding_raises_with_message():
     g = _g(d=96)
     with pytest.raises(S.SpadeError, match="head dim"):
-        S._check(S.lib().spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None))
+        S._check(S.lib().spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None, 0, None))

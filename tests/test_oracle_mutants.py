@@ -106,3 +106,40 @@ def test_softmax_without_max_shift_in_lse_is_caught(monkeypatch):
         return Ob, lse + (lse != 0) * 0.5
     monkeypatch.setattr(O, "block_sparse_attention", lse_off)
     assert _fails(TA.test_matches_eq2_with_explicit_token_mask, G_RAGGED)
+
+
+def test_last_maximum_wins_is_caught(monkeypatch):
+    from . import test_oracle_sweep as TW
+
+    def last_max(as_qk):
+        per_head = np.asarray(as_qk).mean(axis=1)
+        C = per_head.shape[0]
+        choice = C - 1 - np.argmax(per_head[::-1], axis=0)
+        return choice, per_head.max(axis=0)
+    monkeypatch.setattr(O, "choose_schemes", last_max)
+    assert _fails(TW.test_choice_table_by_hand)
+
+
+def test_as_normalised_by_full_block_size_is_caught(monkeypatch):
+    from . import test_oracle_sweep as TW
+
+    def by_bs(sics, g):
+        raw = sics.sum(axis=-1)
+        return raw, raw / float(g.NB * g.BS ** 2)
+    monkeypatch.setattr(O, "aggregation_score", by_bs)
+    assert _fails(TW.test_ragged_tiles_score_one_too)
+
+
+def test_group_output_in_wrong_heads_is_caught(monkeypatch):
+    from . import test_oracle_sweep as TW
+    orig = O.head_groups
+    monkeypatch.setattr(O, "head_groups", lambda choice, C: [list(reversed(h)) for h in orig(choice, C)])
+    orig_attn = O.spade_attention
+
+    def shifted(Q, K, V, g, mode, **kw):
+        r = orig_attn(Q, K, V, g, mode, **kw)
+        r["O"] = np.roll(r["O"], 1, axis=1)
+        return r
+    monkeypatch.setattr(O, "spade_attention", shifted)
+    assert _fails(TW.test_sweep_outputs_land_in_their_heads) or _fails(
+        TW.test_sweep_keeping_every_block_is_dense_attention)
