@@ -1,6 +1,7 @@
 // Flash block-sparse attention (paper Eq. (2), §3.3 optimisation (3)) on gfx950.
 //
 // One workgroup per query block (b, h, i); wave w owns query slots 32w..32w+31.
+// Work items are dealt to the 8 XCDs so that all XCDs share one head at a time.
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
 // chunks of 32 key slots (only chunks that hold real keys).
 //
@@ -110,8 +111,10 @@ __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, con
   }
 }
 
+// From 4 waves per workgroup on, three waves per SIMD (<= 168 VGPRs): two
+// workgroups share a CU. Smaller workgroups keep up to 256 VGPRs (no spills).
 template <int D, int W>
-__global__ void __launch_bounds__(64 * W)
+__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ? 3 : 2)))
     attn_kernel(DevGeom g, const uint4* __restrict__ qb, const char* __restrict__ kb,
                 const char* __restrict__ vb, const int* __restrict__ counts,
                 const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
@@ -122,9 +125,15 @@ __global__ void __launch_bounds__(64 * W)
   lds_char* const lds = (lds_char*)lds_raw;
   lds_int* const list = (lds_int*)list_raw;
 
-  const int64_t item = blockIdx.x;
-  const int64_t bh = item / g.NB;
-  const int i = int(item % g.NB);
+  // Workgroup w runs on XCD w % 8. Every XCD walks the heads in the same order
+  // and takes one contiguous eighth of each head's query blocks: the XCDs work
+  // on the same head at a time (its K/V stays in the MALL) and each XCD's L2
+  // serves spatially adjacent query blocks, whose kept K/V sets overlap.
+  const int per_xcd = (g.NB + 7) / 8;
+  const int64_t slot = int64_t(blockIdx.x) >> 3;
+  const int64_t bh = slot / per_xcd;
+  const int i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
+  if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
   const int n_i = block_ext(g, i).n;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int q0 = wave * 32;
@@ -186,12 +195,21 @@ __global__ void __launch_bounds__(64 * W)
       f32x16 s;
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[r] = 0.0f;
+      {
+        bf16x8 kf[D / 16];
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 a = *(lds_bf16x8*)(Kt + k_off + (((2 * kk + half) ^ k_sw) << 4));
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s, 0, 0, 0);
-      }
-      // s[r]: key (r/4)*8 + 4*half + r%4 of the chunk, query row r32
+        for (int kk = 0; kk < D / 16; ++kk)
+          kf[kk] = *(lds_bf16x8*)(Kt + k_off + (((2 * kk + half) ^ k_sw) << 4));
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], s, 0, 0, 0);
+        // schedule: two K reads ahead of each pair of MFMAs
+#pragma unroll
+        for (int gi = 0; gi < D / 32; ++gi) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS reads
+          __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMAs
+        }
+      }      // s[r]: key (r/4)*8 + 4*half + r%4 of the chunk, query row r32
       if (cur.c0 + kChunk > cur.nj) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -230,20 +248,32 @@ __global__ void __launch_bounds__(64 * W)
           const bf16x2 pr = {p[u][2 * e], p[u][2 * e + 1]};
           l = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l, false);
         }
+      {
+        bf16x8 vf[D / 32][2];
 #pragma unroll
-      for (int t = 0; t < D / 32; ++t) {
+        for (int t = 0; t < D / 32; ++t)
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          bf16x4 h2[2];
+          for (int u = 0; u < 2; ++u) {
+            bf16x4 h2[2];
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int row = 16 * u + 8 * h + v_row0;
-            const int piece = (4 * t + v_piece0) ^ swz_v(row);
-            h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-                (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
+            for (int h = 0; h < 2; ++h) {
+              const int row = 16 * u + 8 * h + v_row0;
+              const int piece = (4 * t + v_piece0) ^ swz_v(row);
+              h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+                  (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
+            }
+            vf[t][u] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
           }
-          const bf16x8 a = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
-          o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, p[u], o[t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+          for (int u = 0; u < 2; ++u)
+            o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][u], p[u], o[t], 0, 0, 0);
+        // schedule: the V^T reads of two output tiles ahead of their four MFMAs
+#pragma unroll
+        for (int gi = 0; gi < D / 64; ++gi) {
+          __builtin_amdgcn_sched_group_barrier(0x100, 8, 1);  // LDS reads
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);  // MFMAs
         }
       }
     }
@@ -283,7 +313,7 @@ template <int D, int W>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                      hipStream_t s) {
-  const int64_t items = int64_t(g.B) * g.H * g.NB;
+  const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
   static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W>),
