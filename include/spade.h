@@ -7,6 +7,8 @@
  *   spade_block_reorder      blocking / layout transform and its inverse
  *                            (optionally for a group of heads, §3.3 (2))
  *   spade_summarize          Summarizer (block means) + optional SICS (§3.2)
+ *   spade_block_summarize    the two above fused into one pass over the raster
+ *                            tensors (§3.3 (1)), optionally for a group of heads
  *   spade_estimate_select    inter-block Estimator + Top-K / Top-P index search
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
@@ -107,6 +109,27 @@ spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y,
 spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb,
                              double* qbar, double* kbar, double* sics_q, double* sics_k,
                              hipStream_t stream);
+
+/*
+ * Blocking, Summarizer and intra-block estimator fused — paper §3.3 optimisation
+ * (1): one pass reads each block's rows of Q and K from the raster layout and
+ * produces what spade_block_reorder (inverse == 0) and spade_summarize produce,
+ * bit for bit for the blocked copies and the same fp64 reductions for the
+ * summaries. With qb/kb NULL nothing is written to the blocked layout: the call
+ * then evaluates a blocking scheme (summaries, SICS) straight from the raster
+ * tensors, as the head-wise scheme choice of §3.2 needs for every candidate.
+ *
+ *   q, k:         raster bf16 [B,H,N,d].
+ *   qb, kb:       out, nullable (both or neither), blocked bf16 [B,n,NB*BS,d].
+ *   qbar, kbar:   out, nullable (both or neither), fp64 [B,n,NB,d].
+ *   sics_q, sics_k: out, nullable (both or neither), fp64 [B,n,NB].
+ *   heads, n_heads: head list as in spade_block_reorder; n = n_heads (H if NULL).
+ *   At least one output pair must be given. Outputs must not alias the inputs.
+ */
+spade_status spade_block_summarize(const spade_geom* g, const void* q, const void* k, void* qb,
+                                   void* kb, double* qbar, double* kbar, double* sics_q,
+                                   double* sics_k, const int32_t* heads, int32_t n_heads,
+                                   hipStream_t stream);
 
 /*
  * Aggregation Score of one blocking-scheme candidate — paper §3.2, Eq. (3):

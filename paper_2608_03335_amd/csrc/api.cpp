@@ -59,6 +59,31 @@ spade_status check_geom(const spade_geom* g, spade::DevGeom* dg, bool* empty) {
   return SPADE_OK;
 }
 
+// Reads a host head list (NULL = all heads) into the by-value map the kernels take.
+spade_status parse_heads(const spade::DevGeom& dg, const int32_t* heads, int32_t n_heads,
+                         spade::HeadMap* hm) {
+  hm->n = dg.H;
+  hm->ident = 1;
+  if (heads == nullptr) {
+    if (n_heads != 0)
+      return fail(SPADE_ERR_INVALID_ARG, "n_heads must be 0 when heads is null (got %d)", n_heads);
+    return SPADE_OK;
+  }
+  if (n_heads < 0 || n_heads > spade::kMaxHeadList)
+    return fail(SPADE_ERR_INVALID_ARG, "n_heads must lie in [0, %d] (got %d)", spade::kMaxHeadList,
+                n_heads);
+  hm->n = n_heads;
+  hm->ident = 0;
+  for (int k = 0; k < n_heads; ++k) {
+    if (heads[k] < 0 || heads[k] >= dg.H)
+      return fail(SPADE_ERR_INVALID_ARG, "heads[%d]=%d outside [0, H=%d)", k, heads[k], dg.H);
+    for (int j = 0; j < k; ++j)
+      if (heads[j] == heads[k]) return fail(SPADE_ERR_INVALID_ARG, "head %d listed twice", heads[k]);
+    hm->h[k] = heads[k];
+  }
+  return SPADE_OK;
+}
+
 spade_status hip_status(hipError_t e, const char* what) {
   if (e == hipSuccess) return SPADE_OK;
   return fail(SPADE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -93,26 +118,8 @@ spade_status spade_block_reorder(const spade_geom* g, const void* x, void* y, in
   if (inverse != 0 && inverse != 1)
     return fail(SPADE_ERR_INVALID_ARG, "inverse must be 0 or 1 (got %d)", inverse);
   spade::HeadMap hm;
-  hm.n = dg.H;
-  hm.ident = 1;
-  if (heads == nullptr) {
-    if (n_heads != 0)
-      return fail(SPADE_ERR_INVALID_ARG, "n_heads must be 0 when heads is null (got %d)", n_heads);
-  } else {
-    if (n_heads < 0 || n_heads > spade::kMaxHeadList)
-      return fail(SPADE_ERR_INVALID_ARG, "n_heads must lie in [0, %d] (got %d)",
-                  spade::kMaxHeadList, n_heads);
-    hm.n = n_heads;
-    hm.ident = 0;
-    for (int k = 0; k < n_heads; ++k) {
-      if (heads[k] < 0 || heads[k] >= dg.H)
-        return fail(SPADE_ERR_INVALID_ARG, "heads[%d]=%d outside [0, H=%d)", k, heads[k], dg.H);
-      for (int j = 0; j < k; ++j)
-        if (heads[j] == heads[k])
-          return fail(SPADE_ERR_INVALID_ARG, "head %d listed twice", heads[k]);
-      hm.h[k] = heads[k];
-    }
-  }
+  st = parse_heads(dg, heads, n_heads, &hm);
+  if (st != SPADE_OK) return st;
   if (empty || hm.n == 0) return SPADE_OK;
   if (!x || !y) return fail(SPADE_ERR_INVALID_ARG, "x and y must be non-null");
   if (!aligned16(x) || !aligned16(y))
@@ -137,6 +144,36 @@ spade_status spade_summarize(const spade_geom* g, const void* qb, const void* kb
     return fail(SPADE_ERR_INVALID_ARG, "qb, kb, qbar and kbar must be 16-byte aligned");
   return hip_status(spade::launch_summarize(dg, qb, kb, qbar, kbar, sics_q, sics_k, stream),
                     "summarize launch");
+}
+
+spade_status spade_block_summarize(const spade_geom* g, const void* q, const void* k, void* qb,
+                                   void* kb, double* qbar, double* kbar, double* sics_q,
+                                   double* sics_k, const int32_t* heads, int32_t n_heads,
+                                   hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if ((qb == nullptr) != (kb == nullptr))
+    return fail(SPADE_ERR_INVALID_ARG, "qb and kb must both be given or both be null");
+  if ((qbar == nullptr) != (kbar == nullptr))
+    return fail(SPADE_ERR_INVALID_ARG, "qbar and kbar must both be given or both be null");
+  if ((sics_q == nullptr) != (sics_k == nullptr))
+    return fail(SPADE_ERR_INVALID_ARG, "sics_q and sics_k must both be given or both be null");
+  if (!qb && !qbar && !sics_q)
+    return fail(SPADE_ERR_INVALID_ARG, "nothing requested: give qb/kb, qbar/kbar or sics_q/sics_k");
+  spade::HeadMap hm;
+  st = parse_heads(dg, heads, n_heads, &hm);
+  if (st != SPADE_OK) return st;
+  if (empty || hm.n == 0) return SPADE_OK;
+  if (!q || !k) return fail(SPADE_ERR_INVALID_ARG, "q and k must be non-null");
+  if (!aligned16(q) || !aligned16(k) || (qb && (!aligned16(qb) || !aligned16(kb))))
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, qb and kb must be 16-byte aligned");
+  if (qb && (qb == q || qb == k || kb == q || kb == k || qb == kb))
+    return fail(SPADE_ERR_INVALID_ARG, "blocked outputs must not alias the inputs or each other");
+  return hip_status(spade::launch_block_summarize(dg, hm, q, k, qb, kb, qbar, kbar, sics_q, sics_k,
+                                                  stream),
+                    "block_summarize launch");
 }
 
 spade_status spade_aggregation_score(const spade_geom* g, const double* sics_q,

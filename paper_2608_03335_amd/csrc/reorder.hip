@@ -14,25 +14,6 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
-template <int VPR>  // 16-byte vectors per token row
-__device__ __forceinline__ int64_t slot_token(const DevGeom& g, const BlockExt& e, float r_ew,
-                                              float r_eh, int slot) {
-  const int q = int((float(slot) + 0.5f) * r_ew);  // slot / ew
-  const int dx = slot - q * e.ew;
-  const int dt = int((float(q) + 0.5f) * r_eh);    // q / eh
-  const int dy = q - dt * e.eh;
-  return (int64_t(e.t0 + dt) * g.Hs + (e.y0 + dy)) * g.Ws + (e.x0 + dx);
-}
-
-// grid.y enumerates (batch, listed head): blocked-side index, raster-side index
-__device__ __forceinline__ void head_pair(const DevGeom& g, const HeadMap& hm, int64_t* blocked,
-                                          int64_t* raster) {
-  const int by = blockIdx.y;
-  const int b = by / hm.n, k = by - b * hm.n;
-  *blocked = by;
-  *raster = int64_t(b) * g.H + (hm.ident ? k : hm.h[k]);
-}
-
 // raster [B, H, N, row] -> blocked [B, n, NB*BS, row]; padding slots get zeros.
 template <int VPR>
 __global__ void __launch_bounds__(kThreads) reorder_fwd(DevGeom g, HeadMap hm,
@@ -55,7 +36,7 @@ __global__ void __launch_bounds__(kThreads) reorder_fwd(DevGeom g, HeadMap hm,
       v[u] = make_uint4(0, 0, 0, 0);
       if (f < valid) {
         const int slot = f / VPR, vec = f % VPR;
-        v[u] = src[slot_token<VPR>(g, e, r_ew, r_eh, slot) * VPR + vec];
+        v[u] = src[block_slot_token(g, e, r_ew, r_eh, slot) * VPR + vec];
       }
     }
 #pragma unroll
@@ -92,7 +73,7 @@ __global__ void __launch_bounds__(kThreads) reorder_inv(DevGeom g, HeadMap hm,
       const int f = f0 + u * kThreads;
       if (f < valid) {
         const int slot = f / VPR, vec = f % VPR;
-        dst[slot_token<VPR>(g, e, r_ew, r_eh, slot) * VPR + vec] = v[u];
+        dst[block_slot_token(g, e, r_ew, r_eh, slot) * VPR + vec] = v[u];
       }
     }
   }

@@ -48,6 +48,28 @@ struct HeadMap {
   int h[kMaxHeadList];
 };
 
+// Raster token of slot `slot` of block e: slots follow raster order of (dt, dy, dx).
+// r_ew = 1/e.ew and r_eh = 1/e.eh; the float quotients are exact because slots and
+// extents stay below 2^8 (see kMaxBS).
+__device__ __forceinline__ int64_t block_slot_token(const DevGeom& g, const BlockExt& e,
+                                                   float r_ew, float r_eh, int slot) {
+  const int q = int((float(slot) + 0.5f) * r_ew);  // slot / ew
+  const int dx = slot - q * e.ew;
+  const int dt = int((float(q) + 0.5f) * r_eh);    // q / eh
+  const int dy = q - dt * e.eh;
+  return (int64_t(e.t0 + dt) * g.Hs + (e.y0 + dy)) * g.Ws + (e.x0 + dx);
+}
+
+// grid.y enumerates (batch, listed head): index on the blocked side (compact over
+// the listed heads) and on the raster side (all H heads).
+__device__ __forceinline__ void head_pair(const DevGeom& g, const HeadMap& hm, int64_t* blocked,
+                                          int64_t* raster) {
+  const int by = blockIdx.y;
+  const int b = by / hm.n, k = by - b * hm.n;
+  *blocked = by;
+  *raster = int64_t(b) * g.H + (hm.ident ? k : hm.h[k]);
+}
+
 // Launchers (each returns hipGetLastError() after its launches).
 hipError_t launch_reorder(const DevGeom& g, const void* x, void* y, int esize, int inverse,
                           const HeadMap& heads, hipStream_t s);
@@ -55,6 +77,9 @@ hipError_t launch_aggregation_score(const DevGeom& g, const double* sics_q, cons
                                     double* as_q, double* as_k, double* as_sum, hipStream_t s);
 hipError_t launch_choose_scheme(const double* as_qk, int C, int B, int H, int* choice,
                                 double* best, hipStream_t s);
+hipError_t launch_block_summarize(const DevGeom& g, const HeadMap& hm, const void* q,
+                                  const void* k, void* qb, void* kb, double* qbar, double* kbar,
+                                  double* sics_q, double* sics_k, hipStream_t s);
 hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
                             double* kbar, double* sics_q, double* sics_k, hipStream_t s);
 hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const double* kbar,

@@ -27,6 +27,17 @@ __device__ __forceinline__ void bf16x8_to_f32(const uint4 v, float f[8]) {
   }
 }
 
+// 1/sqrt(x) for x > 0 in fp64: the hardware estimate (v_rsq_f64) refined by two
+// Newton steps y <- y (3 - x y^2) / 2, each of which squares the relative error;
+// much cheaper than a correctly rounded fp64 sqrt followed by a division.
+__device__ __forceinline__ double inv_sqrt(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+  const double hx = 0.5 * x;
+  y = y * (1.5 - hx * y * y);
+  y = y * (1.5 - hx * y * y);
+  return y;
+}
+
 template <int D, bool SICS>
 __global__ void __launch_bounds__(kThreads) summarize_kernel(DevGeom g, const uint4* __restrict__ qb,
                                                              const uint4* __restrict__ kb,
@@ -63,7 +74,7 @@ __global__ void __launch_bounds__(kThreads) summarize_kernel(DevGeom g, const ui
         for (int k = 0; k < 8; ++k) ss += double(f[k]) * double(f[k]);
 #pragma unroll
         for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
-        const double inv = ss > 0.0 ? 1.0 / sqrt(ss) : 0.0;
+        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
 #pragma unroll
         for (int k = 0; k < 8; ++k) uacc[k] += double(f[k]) * inv;
       }
@@ -101,6 +112,107 @@ __global__ void __launch_bounds__(kThreads) summarize_kernel(DevGeom g, const ui
     // part/upart/sq are rewritten by the next tensor only after this barrier
     __syncthreads();
   }
+}
+
+// Blocking, Summarizer and SICS in one pass over the raster tensors (§3.3
+// optimisation (1)): each workgroup gathers its block's rows of Q, then K, from
+// the raster layout, optionally writes them to the blocked layout (zeros in the
+// padding slots), and reduces them as summarize_kernel does. Grid (block, batch x
+// listed head); summaries and blocked rows are indexed by the listed head.
+template <int D, bool SICS, bool WRITE>
+__global__ void __launch_bounds__(kThreads) block_summarize_kernel(
+    DevGeom g, HeadMap hm, const uint4* __restrict__ q, const uint4* __restrict__ k,
+    uint4* __restrict__ qb, uint4* __restrict__ kb, double* __restrict__ qbar,
+    double* __restrict__ kbar, double* __restrict__ sics_q, double* __restrict__ sics_k) {
+  constexpr int V = D / 8;
+  constexpr int G = kThreads / V;
+  __shared__ double part[G][D];
+  __shared__ double upart[SICS ? G : 1][SICS ? D : 1];
+  __shared__ double sq[kThreads / 64];
+
+  const int b = blockIdx.x;
+  int64_t bh_blk, bh_ras;
+  head_pair(g, hm, &bh_blk, &bh_ras);
+  const BlockExt e = block_ext(g, b);
+  const int n = e.n;
+  const float r_ew = 1.0f / float(e.ew), r_eh = 1.0f / float(e.eh);
+  const int vec = threadIdx.x % V, grp = threadIdx.x / V;
+
+  for (int which = 0; which < 2; ++which) {
+    const uint4* src = (which ? k : q) + bh_ras * g.N * V;
+    uint4* dst = WRITE ? (which ? kb : qb) + (bh_blk * g.NB + b) * int64_t(g.BS) * V : nullptr;
+    double acc[8], uacc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[c] = uacc[c] = 0.0;
+#pragma unroll 2
+    for (int s = grp; s < (WRITE ? g.BS : n); s += G) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (s < n) v = src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec];
+      if (WRITE) dst[int64_t(s) * V + vec] = v;
+      float f[8];
+      bf16x8_to_f32(v, f);  // padding rows are zero: they add nothing below
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[c] += double(f[c]);
+      if (SICS) {
+        double ss = 0.0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) ss += double(f[c]) * double(f[c]);
+#pragma unroll
+        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
+        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) uacc[c] += double(f[c]) * inv;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      part[grp][vec * 8 + c] = acc[c];
+      if (SICS) upart[grp][vec * 8 + c] = uacc[c];
+    }
+    __syncthreads();
+    double u2 = 0.0;
+    if (threadIdx.x < D) {
+      const int c = threadIdx.x;
+      double t = 0.0;
+      for (int r = 0; r < G; ++r) t += part[r][c];
+      double* bar = which ? kbar : qbar;
+      if (bar) bar[(bh_blk * g.NB + b) * D + c] = t / double(n);
+      if (SICS) {
+        double u = 0.0;
+        for (int r = 0; r < G; ++r) u += upart[r][c];
+        u2 = u * u;
+      }
+    }
+    if (SICS) {
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) u2 += __shfl_xor(u2, m, 64);
+      if ((threadIdx.x & 63) == 0) sq[threadIdx.x >> 6] = u2;
+    }
+    __syncthreads();
+    if (SICS && threadIdx.x == 0) {
+      double t = 0.0;
+      for (int w = 0; w < D / 64; ++w) t += sq[w];
+      (which ? sics_k : sics_q)[bh_blk * g.NB + b] = t;
+    }
+    __syncthreads();
+  }
+}
+
+template <int D, bool SICS>
+hipError_t launch_bs(const DevGeom& g, const HeadMap& hm, const void* q, const void* k, void* qb,
+                     void* kb, double* qbar, double* kbar, double* sics_q, double* sics_k,
+                     hipStream_t s) {
+  const dim3 grid(g.NB, g.B * hm.n);
+  const uint4* q4 = static_cast<const uint4*>(q);
+  const uint4* k4 = static_cast<const uint4*>(k);
+  if (qb)
+    block_summarize_kernel<D, SICS, true><<<grid, kThreads, 0, s>>>(
+        g, hm, q4, k4, static_cast<uint4*>(qb), static_cast<uint4*>(kb), qbar, kbar, sics_q,
+        sics_k);
+  else
+    block_summarize_kernel<D, SICS, false><<<grid, kThreads, 0, s>>>(
+        g, hm, q4, k4, nullptr, nullptr, qbar, kbar, sics_q, sics_k);
+  return hipGetLastError();
 }
 
 template <int D>
@@ -187,6 +299,18 @@ hipError_t launch_aggregation_score(const DevGeom& g, const double* sics_q, cons
   aggregation_score_kernel<<<dim3(g.B * g.H), kThreads, 0, s>>>(g, sics_q, sics_k, as_q, as_k,
                                                                  as_sum);
   return hipGetLastError();
+}
+
+hipError_t launch_block_summarize(const DevGeom& g, const HeadMap& hm, const void* q,
+                                  const void* k, void* qb, void* kb, double* qbar, double* kbar,
+                                  double* sics_q, double* sics_k, hipStream_t s) {
+  if (g.d == 128)
+    return sics_q ? launch_bs<128, true>(g, hm, q, k, qb, kb, qbar, kbar, sics_q, sics_k, s)
+                  : launch_bs<128, false>(g, hm, q, k, qb, kb, qbar, kbar, nullptr, nullptr, s);
+  if (g.d == 64)
+    return sics_q ? launch_bs<64, true>(g, hm, q, k, qb, kb, qbar, kbar, sics_q, sics_k, s)
+                  : launch_bs<64, false>(g, hm, q, k, qb, kb, qbar, kbar, nullptr, nullptr, s);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,

@@ -1,8 +1,11 @@
-"""Buffers + the five C-ABI calls of one sparse attention pass (paper §3.3 order).
+"""Buffers + the C-ABI calls of one sparse attention pass (paper §3.3 order).
 
 blocking (Q, K, V) -> summaries -> estimate + select -> block-sparse attention
--> restore layout. All buffers are allocated once here (torch, device memory);
-`run` only issues the library calls on one stream, with no host sync.
+-> restore layout. By default the blocking of Q and K and their summaries are
+one fused call (spade_block_summarize, §3.3 optimisation (1)); `fused=False`
+issues spade_block_reorder x3 + spade_summarize instead. All buffers are
+allocated once here (torch, device memory); `run` only issues the library calls
+on one stream, with no host sync.
 """
 from __future__ import annotations
 
@@ -25,8 +28,9 @@ def block_valid_counts(g) -> np.ndarray:
 
 class SpadePath:
     def __init__(self, B, H, d, T, Hs, Ws, bt, bh, bw, *, mode="topp", topk=None, tau=None,
-                 scale=None, device="cuda", with_sics=False, with_lse=False):
+                 scale=None, device="cuda", with_sics=False, with_lse=False, fused=True):
         self.g = S.geom(B, H, d, T, Hs, Ws, bt, bh, bw)
+        self.fused = bool(fused)
         self.mode = S.SPADE_TOPP if mode == "topp" else S.SPADE_TOPK
         self.topk = int(topk or 0)
         self.tau = float(tau if tau is not None else 1.0)
@@ -51,10 +55,19 @@ class SpadePath:
 
     # individual stages, so they can be timed separately
     def reorder_in(self, Q, K, V, stream=None):
+        """Blocking of Q, K, V; in fused mode also the summaries of Q and K."""
+        if self.fused:
+            S.spade_block_summarize(self.g, Q, K, self.Qb, self.Kb, self.qbar, self.kbar,
+                                    self.sics_q, self.sics_k, stream=stream)
+            S.spade_block_reorder(self.g, V, self.Vb, inverse=False, stream=stream)
+            return
         for x, y in ((Q, self.Qb), (K, self.Kb), (V, self.Vb)):
             S.spade_block_reorder(self.g, x, y, inverse=False, stream=stream)
 
     def summarize(self, stream=None):
+        """Summaries of the blocked Q, K (already produced by reorder_in in fused mode)."""
+        if self.fused:
+            return
         S.spade_summarize(self.g, self.Qb, self.Kb, self.qbar, self.kbar, self.sics_q,
                           self.sics_k, stream=stream)
 
@@ -87,12 +100,14 @@ def _chunks(heads, n):
 class SweepPath:
     """Head-wise blocking choice over candidate schemes, then one path per head group.
 
-    Evaluation (§3.2): for every candidate, blocking of Q and K for all heads,
-    summaries with SICS, the normalised Aggregation Score, then the per-head
-    argmax on the device. The choice is read back to the host (the one sync) to
-    form the head groups; each group then runs blocking with its head list
-    (§3.3 (2)), summaries, Top-K selection with k = max(1, round((1 - s) NB)),
-    block-sparse attention and the inverse blocking into the full output.
+    Evaluation (§3.2): for every candidate, SICS of Q and K straight from the
+    raster tensors (fused call, nothing written in blocked layout), the
+    normalised Aggregation Score, then the per-head argmax on the device. The
+    choice is read back to the host (the one sync) to form the head groups; each
+    group then runs the fused blocking + summaries of Q, K with its head list
+    (§3.3 (1), (2)), the blocking of V, Top-K selection with
+    k = max(1, round((1 - s) NB)), block-sparse attention and the inverse
+    blocking into the full output.
     """
 
     def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda"):
@@ -103,17 +118,10 @@ class SweepPath:
         self.geoms = [S.geom(B, H, d, T, Hs, Ws, *c) for c in self.shapes]
         bf, f64, dev = torch.bfloat16, torch.float64, device
         self.topk = [max(1, int(math.floor((1.0 - self.sparsity) * g.NB + 0.5))) for g in self.geoms]
-        # evaluation buffers, one set per candidate (all heads)
-        self.ev = []
-        for g in self.geoms:
-            rows = g.NB * g.BS
-            self.ev.append(dict(
-                Qb=torch.empty((B, H, rows, d), dtype=bf, device=dev),
-                Kb=torch.empty((B, H, rows, d), dtype=bf, device=dev),
-                qbar=torch.empty((B, H, g.NB, d), dtype=f64, device=dev),
-                kbar=torch.empty((B, H, g.NB, d), dtype=f64, device=dev),
-                sics_q=torch.empty((B, H, g.NB), dtype=f64, device=dev),
-                sics_k=torch.empty((B, H, g.NB), dtype=f64, device=dev)))
+        # evaluation buffers, one set per candidate (all heads): SICS only
+        self.ev = [dict(sics_q=torch.empty((B, H, g.NB), dtype=f64, device=dev),
+                        sics_k=torch.empty((B, H, g.NB), dtype=f64, device=dev))
+                   for g in self.geoms]
         C = len(self.geoms)
         self.as_qk = torch.empty((C, B, H), dtype=f64, device=dev)
         self.choice = torch.empty(H, dtype=torch.int32, device=dev)
@@ -139,10 +147,7 @@ class SweepPath:
 
     def evaluate(self, Q, K, stream=None):
         for c, (g, e) in enumerate(zip(self.geoms, self.ev)):
-            S.spade_block_reorder(g, Q, e["Qb"], stream=stream)
-            S.spade_block_reorder(g, K, e["Kb"], stream=stream)
-            S.spade_summarize(g, e["Qb"], e["Kb"], e["qbar"], e["kbar"], e["sics_q"], e["sics_k"],
-                              stream=stream)
+            S.spade_block_summarize(g, Q, K, sics_q=e["sics_q"], sics_k=e["sics_k"], stream=stream)
             S.spade_aggregation_score(g, e["sics_q"], e["sics_k"], self.as_qk[c], stream=stream)
         S.spade_choose_scheme(self.as_qk, self.choice, self.best, stream=stream)
 
@@ -169,9 +174,9 @@ class SweepPath:
     # group stages, separately callable so they can be timed
     def group_select(self, c, heads, Q, K, V, stream=None):
         g, v = self.geoms[c], self.group_views(c, len(heads))
-        for x, key in ((Q, "Q"), (K, "K"), (V, "V")):
-            S.spade_block_reorder(g, x, v[key], heads=heads, stream=stream)
-        S.spade_summarize(v["g"], v["Q"], v["K"], v["qbar"], v["kbar"], stream=stream)
+        S.spade_block_summarize(g, Q, K, v["Q"], v["K"], v["qbar"], v["kbar"], heads=heads,
+                                stream=stream)
+        S.spade_block_reorder(g, V, v["V"], heads=heads, stream=stream)
         S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
                                 self.scale, v["counts"], v["indices"], stream=stream)
         return v

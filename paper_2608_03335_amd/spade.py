@@ -18,7 +18,8 @@ SPADE_OK, SPADE_ERR_INVALID_ARG, SPADE_ERR_UNSUPPORTED, SPADE_ERR_WORKSPACE, SPA
 SPADE_BF16, SPADE_FP32 = 0, 1
 SPADE_TOPK, SPADE_TOPP = 0, 1
 
-EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_aggregation_score",
+EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
+            "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_status_string", "spade_last_error")
 MAX_HEAD_LIST = 64
@@ -66,6 +67,8 @@ def lib() -> ctypes.CDLL:
         sig = {
             "spade_block_reorder": (i32, [G, vp, vp, i32, i32, ctypes.POINTER(i32), i32, vp]),
             "spade_summarize": (i32, [G, vp, vp, vp, vp, vp, vp, vp]),
+            "spade_block_summarize": (i32, [G, vp, vp, vp, vp, vp, vp, vp, vp,
+                                            ctypes.POINTER(i32), i32, vp]),
             "spade_aggregation_score": (i32, [G, vp, vp, vp, vp, vp, vp]),
             "spade_choose_scheme": (i32, [vp, i32, i32, i32, vp, vp, vp]),
             "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
@@ -116,6 +119,13 @@ def spade_block_reorder(g: spade_geom, x, y, inverse: bool = False, heads=None, 
 def spade_summarize(g: spade_geom, qb, kb, qbar, kbar, sics_q=None, sics_k=None, stream=None):
     _check(lib().spade_summarize(ctypes.byref(g), _p(qb), _p(kb), _p(qbar), _p(kbar),
                                  _p(sics_q), _p(sics_k), _s(stream)))
+
+
+def spade_block_summarize(g: spade_geom, q, k, qb=None, kb=None, qbar=None, kbar=None,
+                          sics_q=None, sics_k=None, heads=None, stream=None):
+    arr, n = _head_list(heads)
+    _check(lib().spade_block_summarize(ctypes.byref(g), _p(q), _p(k), _p(qb), _p(kb), _p(qbar),
+                                       _p(kbar), _p(sics_q), _p(sics_k), arr, n, _s(stream)))
 
 
 def spade_aggregation_score(g: spade_geom, sics_q, sics_k, as_qk, as_q=None, as_k=None,

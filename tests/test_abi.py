@@ -24,7 +24,8 @@ def _declared():
 def test_header_declares_the_path_calls():
     names = _declared()
     for n in ("spade_block_reorder", "spade_summarize", "spade_estimate_select",
-              "spade_block_sparse_attn", "spade_aggregation_score", "spade_choose_scheme"):
+              "spade_block_sparse_attn", "spade_aggregation_score", "spade_choose_scheme",
+              "spade_block_summarize"):
         assert n in names
 
 
@@ -106,6 +107,27 @@ def test_reorder_head_list_errors(heads, n, expect):
         assert st == expect, (heads, n, inverse)
 
 
+def test_block_summarize_errors():
+    L = S.lib()
+    g = _g()
+    B2 = ctypes.c_void_p(0x2000)
+    call = lambda *a: L.spade_block_summarize(ctypes.byref(g), *a)
+    # pairs must come together; something must be requested
+    assert call(FAKE, B2, FAKE, NULL, NULL, NULL, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, B2, NULL, NULL, FAKE, NULL, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, B2, NULL, NULL, NULL, NULL, FAKE, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, B2, NULL, NULL, NULL, NULL, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    # null or misaligned inputs, aliasing outputs
+    assert call(NULL, B2, NULL, NULL, FAKE, FAKE, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, MISALIGNED, NULL, NULL, FAKE, FAKE, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, B2, FAKE, ctypes.c_void_p(0x3000), NULL, NULL, NULL, NULL, None, 0, None) == S.SPADE_ERR_INVALID_ARG
+    # head list checks as for the reorder
+    assert call(FAKE, B2, NULL, NULL, FAKE, FAKE, NULL, NULL, _heads(0, 2), 2, None) == S.SPADE_ERR_INVALID_ARG
+    assert call(FAKE, B2, NULL, NULL, FAKE, FAKE, NULL, NULL, None, 1, None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_block_summarize(ctypes.byref(_g(d=96)), FAKE, B2, NULL, NULL, FAKE, FAKE, NULL,
+                                   NULL, None, 0, None) == S.SPADE_ERR_UNSUPPORTED
+
+
 def test_aggregation_and_choice_errors():
     L = S.lib()
     g = _g()
@@ -128,6 +150,8 @@ def test_empty_problem_is_a_no_op():
         assert L.spade_block_reorder(ctypes.byref(g), NULL, NULL, 0, 0, None, 0, None) == S.SPADE_OK
         assert L.spade_summarize(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, NULL, None) == S.SPADE_OK
         assert L.spade_aggregation_score(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, None) == S.SPADE_OK
+        assert L.spade_block_summarize(ctypes.byref(g), NULL, NULL, NULL, NULL, FAKE, FAKE, NULL, NULL,
+                                       None, 0, None) == S.SPADE_OK
         assert L.spade_estimate_select(ctypes.byref(g), NULL, NULL, 0, 1, 0.0, 1.0, NULL, NULL, NULL, None) == S.SPADE_OK
         assert L.spade_attn_workspace_bytes(ctypes.byref(g)) == 0
         assert L.spade_block_sparse_attn(ctypes.byref(g), NULL, NULL, NULL, NULL, NULL, 1.0,
