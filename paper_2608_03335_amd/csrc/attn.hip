@@ -1,6 +1,7 @@
 // Flash block-sparse attention (paper Eq. (2), §3.3 optimisation (3)) on gfx950.
 //
-// One workgroup per query block (b, h, i); wave w owns query slots 32w..32w+31.
+// One workgroup per query block (b, h, i); wave w owns query slots 32w..32w+31;
+// for most block sizes one more wave only issues the K/V loads.
 // Work items are dealt to the 8 XCDs so that all XCDs share one head at a time.
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
 // chunks of 32 key slots (only chunks that hold real keys).
@@ -111,10 +112,39 @@ __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, con
   }
 }
 
-// From 4 waves per workgroup on, three waves per SIMD (<= 168 VGPRs): two
-// workgroups share a CU. Smaller workgroups keep up to 256 VGPRs (no spills).
-template <int D, int W>
-__global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >= 4 ? 3 : 2)))
+// Loader-wave variant: one extra wave issues all 2*LOADS loads of a chunk, so
+// the compute waves never wait on load issue or address arithmetic. The chunk
+// base is uniform (an SGPR pair); each lane adds its 32-bit row/piece offset.
+template <int D>
+__device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, const char* vb,
+                                             int64_t head_row, const Cursor& c,
+                                             uint32_t lds_buf, int lane) {
+  using TL = Tile<D>;
+  const int64_t row_bytes = (head_row + int64_t(c.j) * g.BS + c.c0) * TL::ROW_BYTES;
+  const char* kbase = kb + row_bytes;
+  const char* vbase = vb + row_bytes;
+  const int last = c.nj - 1 - c.c0;  // last real key slot of the chunk
+#pragma unroll
+  for (int q = 0; q < 2 * TL::LOADS; ++q) {
+    const bool is_v = q >= TL::LOADS;
+    const int qq = is_v ? q - TL::LOADS : q;
+    const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
+    const int gp = (lane % TL::NCH) ^ (is_v ? swz_v(r) : swz_k<D>(r));
+    const uint32_t off = uint32_t(min(r, last) * TL::ROW_BYTES + gp * 16);
+    const uint32_t dst = lds_buf + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;  // M0
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(is_v ? vbase : kbase),
+                 "{m0}"(dst)
+                 : "memory");
+  }
+}
+
+// W compute waves (32 query slots each), plus one loader wave when LD. The
+// workgroup shapes are chosen so that a CU holds 12 waves at three waves per
+// SIMD (<= 168 VGPRs): 4 compute waves without a loader (3 workgroups per CU),
+// 5 compute waves with one (2 workgroups of 6).
+template <int D, int W, bool LD>
+__global__ void __launch_bounds__(64 * (W + LD))
+    __attribute__((amdgpu_waves_per_eu(W + LD >= 3 ? 3 : 2)))
     attn_kernel(DevGeom g, const uint4* __restrict__ qb, const char* __restrict__ kb,
                 const char* __restrict__ vb, const int* __restrict__ counts,
                 const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
@@ -135,7 +165,9 @@ __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >
   const int i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
   if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
   const int n_i = block_ext(g, i).n;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep in an SGPR
+  const bool loader = LD && wave == W;  // loader wave: q0 = 32 W >= BS, so no query rows
   const int q0 = wave * 32;
   const int half = lane >> 5;  // k-slot group of the MFMA operands
   const int r32 = lane & 31;
@@ -157,7 +189,7 @@ __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >
   const int cnt = min(max(counts[bh * g.NB + i], 0), g.NB);
   {
     const int* src = indices + (bh * g.NB + i) * int64_t(g.NB);
-    for (int e = threadIdx.x; e < cnt; e += 64 * W) list[e] = src[e];
+    for (int e = threadIdx.x; e < cnt; e += 64 * (W + LD)) list[e] = src[e];
   }
   __syncthreads();  // list visible to every wave (also completes the Q loads)
 
@@ -180,15 +212,25 @@ __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >
   const bool rows_live = q0 < n_i;
   const bf16x2 ones = {__bf16(1.0f), __bf16(1.0f)};
 
+  const uint32_t lds_u32 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  // issue the loads of chunk c into buffer b (all of them from the loader wave,
+  // or each wave its share)
+  auto issue = [&](const Cursor& c, int b) {
+    if (LD) {
+      if (loader) loader_chunk<D>(g, kb, vb, head_row, c, lds_u32 + b * TL::BUF_BYTES, lane);
+    } else {
+      load_chunk<D, W>(g, kb, vb, head_row, c, lds + b * TL::BUF_BYTES, wave, lane);
+    }
+  };
   Cursor cur = {-1, 0, 0, -kChunk};
   cur = next_chunk(g, list, cnt, cur);
   int buf = 0;
-  if (cur.jj < cnt) load_chunk<D, W>(g, kb, vb, head_row, cur, lds, wave, lane);
+  if (cur.jj < cnt) issue(cur, 0);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   while (cur.jj < cnt) {
     const Cursor nxt = next_chunk(g, list, cnt, cur);
-    if (nxt.jj < cnt) load_chunk<D, W>(g, kb, vb, head_row, nxt, lds + (buf ^ 1) * TL::BUF_BYTES, wave, lane);
+    if (nxt.jj < cnt) issue(nxt, buf ^ 1);
     if (rows_live) {
       lds_char* Kt = lds + buf * TL::BUF_BYTES;
       lds_char* Vt = Kt + TL::TILE_BYTES;
@@ -309,20 +351,20 @@ __global__ void __launch_bounds__(64 * W) __attribute__((amdgpu_waves_per_eu(W >
   }
 }
 
-template <int D, int W>
+template <int D, int W, bool LD>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                      hipStream_t s) {
   const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
   static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W, LD>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        int(kMaxAttnNB * sizeof(int)));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  attn_kernel<D, W><<<dim3(unsigned(items)), 64 * W, size_t(g.NB) * sizeof(int), s>>>(
+  attn_kernel<D, W, LD><<<dim3(unsigned(items)), 64 * (W + LD), size_t(g.NB) * sizeof(int), s>>>(
       g, static_cast<const uint4*>(qb), static_cast<const char*>(kb),
       static_cast<const char*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
   return hipGetLastError();
@@ -332,15 +374,16 @@ template <int D>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                     hipStream_t s) {
+  // loader wave unless it would cost a workgroup per CU (4 or 6 compute waves)
   switch ((g.BS + 31) / 32) {
-    case 1: return launch_dw<D, 1>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 2: return launch_dw<D, 2>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 3: return launch_dw<D, 3>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 4: return launch_dw<D, 4>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 5: return launch_dw<D, 5>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 6: return launch_dw<D, 6>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 7: return launch_dw<D, 7>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 8: return launch_dw<D, 8>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 1: return launch_dw<D, 1, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 2: return launch_dw<D, 2, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 3: return launch_dw<D, 3, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 4: return launch_dw<D, 4, false>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 5: return launch_dw<D, 5, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 6: return launch_dw<D, 6, false>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 7: return launch_dw<D, 7, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    case 8: return launch_dw<D, 8, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
   }
   return hipErrorInvalidValue;
 }
