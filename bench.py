@@ -66,6 +66,10 @@ def stage_bytes(p: SpadePath, nvalid: np.ndarray) -> dict:
     N, NBS = g.N, g.NB * g.BS
     kept_entries = float(p.counts.sum().item())
     summaries = 2.0 * g.NB * d * 8
+    if p.virtual:
+        # summaries straight from the raster Q, K; nothing is blocked or restored
+        return {"summaries": BH * (2.0 * N * row + summaries),
+                "select": BH * (summaries + g.NB * 4) + kept_entries * 4}
     if p.fused:
         stages = {
             # Q, K: read every raster row once, write every blocked slot (padding as
@@ -237,6 +241,9 @@ def main():
     ap.add_argument("--no-dense", action="store_true", help="skip the full-mask baseline")
     ap.add_argument("--cpu-budget", type=float, default=15.0,
                     help="seconds of oracle attention in the CPU baseline (0 = skip)")
+    ap.add_argument("--layout", default="raster", choices=["raster", "blocked"],
+                    help="raster: attention gathers rows from the raster tensors (no blocked "
+                         "copies); blocked: blocking + summaries pass, blocked attention, restore")
     ap.add_argument("--sweep", action="store_true",
                     help="run the block-shape sweep (per-head blocking choice) instead")
     ap.add_argument("--copy-calib", action="store_true",
@@ -268,7 +275,7 @@ def main():
     Q, K, V = (x.to(torch.bfloat16) for x in make_inputs(cfg, seed=0, device=dev))
     p = SpadePath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"],
                   cfg["bh"], cfg["bw"], mode=cfg["mode"], topk=cfg.get("topk"),
-                  tau=cfg.get("tau"), device=dev)
+                  tau=cfg.get("tau"), device=dev, virtual=args.layout == "raster")
     g = p.g
     nvalid_np = block_valid_counts(g)
     nvalid = torch.from_numpy(nvalid_np).to(dev)
@@ -306,7 +313,11 @@ def main():
     names = ["reorder", "summarize", "select", "attention", "restore"]
     stage_ms = {n: float(np.mean([ev[k][s].elapsed_time(ev[k][s + 1]) for k in range(K_)]))
                 for s, n in enumerate(names)}
-    if p.fused:  # blocking of Q, K, V and the summaries are one stage
+    if p.virtual:  # summaries from raster; attention reads and writes raster rows
+        stage_ms["summaries"] = stage_ms.pop("reorder") + stage_ms.pop("summarize")
+        stage_ms.pop("restore")
+        names = ["summaries", "select", "attention"]
+    elif p.fused:  # blocking of Q, K, V and the summaries are one stage
         stage_ms["blocking_summaries"] = stage_ms.pop("reorder") + stage_ms.pop("summarize")
         names = ["blocking_summaries", "select", "attention", "restore"]
 
@@ -368,7 +379,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded smooth-field + noise Q/K/V, bf16, resident in HBM)",
-        "config": {"workload": WORKLOAD_LABEL[args.workload], "B": g.B, "H": g.H, "d": g.d,
+        "config": {"workload": WORKLOAD_LABEL[args.workload], "layout": args.layout,
+                   "B": g.B, "H": g.H, "d": g.d,
                    "grid": [g.T, g.Hs, g.Ws], "block": [g.bt, g.bh, g.bw], "N": g.N,
                    "NB": g.NB, "selection": cfg["mode"] + (f" tau={cfg['tau']}" if cfg["mode"] == "topp"
                                                             else f" k={cfg['topk']}"),

@@ -11,6 +11,7 @@
  *                            tensors (§3.3 (1)), optionally for a group of heads
  *   spade_estimate_select    inter-block Estimator + Top-K / Top-P index search
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
+ *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
  *   spade_aggregation_score  per-head Aggregation Score of one candidate scheme
  *   spade_choose_scheme      per-head argmax over the candidates
@@ -216,6 +217,25 @@ spade_status spade_block_sparse_attn(const spade_geom* g, const void* qb, const 
                                      const int32_t* indices, double scale, void* ob, float* lse,
                                      void* workspace, size_t workspace_bytes,
                                      hipStream_t stream);
+
+/*
+ * Flash block-sparse attention on raster tensors — the same computation as
+ * spade_block_sparse_attn, with the blocking applied while reading (each key or
+ * query slot is fetched from its raster token) and the output written back in
+ * raster order: §3.3's rearrangement and restoration without blocked copies.
+ *
+ *   q, k, v: raster bf16 [B,H,N,d].
+ *   counts, indices, scale, workspace: as for spade_block_sparse_attn.
+ *   o:       out, raster bf16 [B,H,N,d]; every token row is written.
+ *   lse:     out, nullable, fp32 [B,H,N].
+ *   Requires N*d*2 < 2^31 (one head's rows addressable with 32-bit offsets).
+ *   Results equal spade_block_sparse_attn's on the blocked copies, bit for bit.
+ */
+spade_status spade_sparse_attn_raster(const spade_geom* g, const void* q, const void* k,
+                                      const void* v, const int32_t* counts,
+                                      const int32_t* indices, double scale, void* o, float* lse,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* spade_status_string(spade_status s);

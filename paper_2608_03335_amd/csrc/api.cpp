@@ -89,6 +89,34 @@ spade_status hip_status(hipError_t e, const char* what) {
   return fail(SPADE_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+spade_status sparse_attn(const spade_geom* g, const void* q, const void* k, const void* v,
+                         const int32_t* counts, const int32_t* indices, double scale, void* o,
+                         float* lse, void* workspace, size_t workspace_bytes, bool raster,
+                         hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (!(isfinite(scale) && scale > 0.0))
+    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
+  if (!empty && dg.NB > spade::kMaxAttnNB)
+    return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the attention limit %d", dg.NB,
+                spade::kMaxAttnNB);
+  if (!empty && raster && dg.N * int64_t(dg.d) * 2 >= (int64_t(1) << 31))
+    return fail(SPADE_ERR_UNSUPPORTED, "raster attention needs N*d*2 < 2^31 bytes per head");
+  if (empty) return SPADE_OK;
+  if (!q || !k || !v || !counts || !indices || !o)
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, v, counts, indices and o must be non-null");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  const size_t need = spade::attn_workspace_bytes(dg);
+  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace_bytes);
+  return hip_status(spade::launch_block_sparse_attn(dg, q, k, v, counts, indices, float(scale), o,
+                                                    lse, workspace, raster, stream),
+                    "sparse attention launch");
+}
 }  // namespace
 
 extern "C" {
@@ -245,27 +273,17 @@ spade_status spade_block_sparse_attn(const spade_geom* g, const void* qb, const 
                                      const int32_t* indices, double scale, void* ob, float* lse,
                                      void* workspace, size_t workspace_bytes,
                                      hipStream_t stream) {
-  spade::DevGeom dg;
-  bool empty = false;
-  spade_status st = check_geom(g, &dg, &empty);
-  if (st != SPADE_OK) return st;
-  if (!(isfinite(scale) && scale > 0.0))
-    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
-  if (!empty && dg.NB > spade::kMaxAttnNB)
-    return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the attention limit %d", dg.NB,
-                spade::kMaxAttnNB);
-  if (empty) return SPADE_OK;
-  if (!qb || !kb || !vb || !counts || !indices || !ob)
-    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, vb, counts, indices and ob must be non-null");
-  if (!aligned16(qb) || !aligned16(kb) || !aligned16(vb) || !aligned16(ob))
-    return fail(SPADE_ERR_INVALID_ARG, "qb, kb, vb and ob must be 16-byte aligned");
-  const size_t need = spade::attn_workspace_bytes(dg);
-  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
-    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
-                workspace_bytes);
-  return hip_status(spade::launch_block_sparse_attn(dg, qb, kb, vb, counts, indices, float(scale),
-                                                    ob, lse, workspace, stream),
-                    "block_sparse_attn launch");
+  return sparse_attn(g, qb, kb, vb, counts, indices, scale, ob, lse, workspace, workspace_bytes,
+                     false, stream);
+}
+
+spade_status spade_sparse_attn_raster(const spade_geom* g, const void* q, const void* k,
+                                      const void* v, const int32_t* counts,
+                                      const int32_t* indices, double scale, void* o, float* lse,
+                                      void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+  return sparse_attn(g, q, k, v, counts, indices, scale, o, lse, workspace, workspace_bytes, true,
+                     stream);
 }
 
 }  // extern "C"

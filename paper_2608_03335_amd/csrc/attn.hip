@@ -64,10 +64,37 @@ __device__ __forceinline__ int swz_k(int r) { return r & (Tile<D>::NCH - 1); }
 __device__ __forceinline__ int swz_v(int r) { return 2 * (r & 3); }
 
 // Position in the kept-block walk: list entry jj, its block j and real-key count nj,
-// and the chunk's first key slot c0.
+// the chunk's first key slot c0, and block j's extent (raster addressing).
 struct Cursor {
   int jj, j, nj, c0;
+  BlockExt e;
 };
+
+// Raster token of slot `slot` of a block of any extent (ragged edge blocks).
+__device__ __forceinline__ int64_t ext_token(const DevGeom& g, const BlockExt& e, int slot) {
+  return block_slot_token(g, e, __builtin_amdgcn_rcpf(float(e.ew)),
+                          __builtin_amdgcn_rcpf(float(e.eh)), slot);
+}
+
+// Raster token of a block's first slot.
+__device__ __forceinline__ int64_t block_origin(const DevGeom& g, const BlockExt& e) {
+  return (int64_t(e.t0) * g.Hs + e.y0) * g.Ws + e.x0;
+}
+
+// Raster addressing of slot s of the cursor's block, relative to `base`: full
+// blocks (every block away from the grid's far edges) share one slot -> token
+// offset table `rel` (LDS, built once per workgroup), so a load costs one LDS
+// read instead of the division-based map; ragged blocks take the map.
+struct RasterRows {
+  bool full;
+  int64_t base;  // head_row + block origin (full), head_row (ragged)
+};
+
+__device__ __forceinline__ RasterRows raster_rows(const DevGeom& g, const Cursor& c,
+                                                  int64_t head_row) {
+  const bool full = c.e.n == g.BS;
+  return {full, head_row + (full ? block_origin(g, c.e) : 0)};
+}
 
 __device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const lds_int* list, int cnt,
                                              Cursor c) {
@@ -82,55 +109,109 @@ __device__ __forceinline__ Cursor next_chunk(const DevGeom& g, const lds_int* li
     const int j = __builtin_amdgcn_readfirstlane(list[c.jj]);  // uniform: keep in SGPRs
     if (j >= 0 && j < g.NB) {
       c.j = j;
-      c.nj = block_ext(g, j).n;
+      c.e = block_ext(g, j);
+      c.nj = c.e.n;
       c.c0 = 0;
     }
   }
   return c;
 }
 
-// Issue this wave's share of the 16-byte global->LDS loads of one chunk.
+// Loads of one chunk without a loader wave: wave w issues loads w, w + W, ...
+// of the 2*LOADS (K tiles, then V). wave_rows gives each of them its row
+// relative to the chunk's base row (blocked: the block's first row; RASTER: the
+// head's first raster row, plus the block origin for full blocks); it is called
+// one chunk ahead, so its LDS table reads complete under the current chunk's math.
 template <int D, int W>
+struct WaveLoads {
+  static constexpr int NQ = (2 * Tile<D>::LOADS + W - 1) / W;  // loads per wave (at most)
+};
+
+template <int D, int W, bool RASTER>
+__device__ __forceinline__ void wave_rows(const DevGeom& g, const Cursor& c, const lds_int* rel,
+                                          int wave, int lane, int (&rows)[WaveLoads<D, W>::NQ]) {
+  using TL = Tile<D>;
+  const int last = c.nj - 1 - c.c0;  // last real key slot of the chunk
+  auto fill = [&](auto row_of) {
+#pragma unroll
+    for (int k = 0; k < WaveLoads<D, W>::NQ; ++k) {
+      const int qq = (wave + k * W) % TL::LOADS;
+      rows[k] = row_of(c.c0 + min(qq * TL::RPI + lane / TL::NCH, last));
+    }
+  };
+  if (!RASTER)
+    fill([](int s) { return s; });
+  else if (c.e.n == g.BS)
+    fill([&](int s) { return rel[s]; });
+  else
+    fill([&](int s) { return int(ext_token(g, c.e, s)); });
+}
+
+template <int D, int W, bool RASTER>
 __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, const char* vb,
-                                           int64_t head_row, const Cursor& c, lds_char* buf,
+                                           int64_t head_row, const Cursor& c,
+                                           const int (&rows)[WaveLoads<D, W>::NQ], lds_char* buf,
                                            int wave, int lane) {
   using TL = Tile<D>;
-  const int64_t blk_row = head_row + int64_t(c.j) * g.BS + c.c0;
-  const int last = c.nj - 1 - c.c0;  // last real key slot of the chunk
+  const int64_t base = RASTER ? raster_rows(g, c, head_row).base
+                              : head_row + int64_t(c.j) * g.BS;
   const int piece = lane % TL::NCH;
 #pragma unroll
-  for (int q = wave; q < 2 * TL::LOADS; q += W) {
-    const bool is_v = q >= TL::LOADS;
-    const int qq = is_v ? q - TL::LOADS : q;
-    const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
-    const int src_r = min(r, last);
-    const int gp = piece ^ (is_v ? swz_v(r) : swz_k<D>(r));
-    const char* src = (is_v ? vb : kb) + (blk_row + src_r) * TL::ROW_BYTES + gp * 16;
-    const uint32_t dst =  // M0: LDS base of this wave-wide 1 KB load
-        uint32_t(reinterpret_cast<uintptr_t>(buf)) + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
-    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(dst) : "memory");
+  for (int k = 0; k < WaveLoads<D, W>::NQ; ++k) {
+    const int q = wave + k * W;
+    if (q < 2 * TL::LOADS) {
+      const bool is_v = q >= TL::LOADS;
+      const int qq = is_v ? q - TL::LOADS : q;
+      const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
+      const int gp = piece ^ (is_v ? swz_v(r) : swz_k<D>(r));
+      const char* src = (is_v ? vb : kb) + (base + rows[k]) * TL::ROW_BYTES + gp * 16;
+      const uint32_t dst =  // M0: LDS base of this wave-wide 1 KB load
+          uint32_t(reinterpret_cast<uintptr_t>(buf)) + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
+      asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(dst) : "memory");
+    }
   }
 }
 
 // Loader-wave variant: one extra wave issues all 2*LOADS loads of a chunk, so
 // the compute waves never wait on load issue or address arithmetic. The chunk
 // base is uniform (an SGPR pair); each lane adds its 32-bit row/piece offset.
-template <int D>
+// RASTER: the base is the head's first raster row (plus the block origin for
+// full blocks) and the offset carries the slot's raster token (the head's rows
+// span < 2^31 bytes, checked on the host); a lane's K and V rows are the same,
+// so each offset is computed once.
+template <int D, bool RASTER>
 __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, const char* vb,
-                                             int64_t head_row, const Cursor& c,
+                                             int64_t head_row, const Cursor& c, const lds_int* rel,
                                              uint32_t lds_buf, int lane) {
   using TL = Tile<D>;
-  const int64_t row_bytes = (head_row + int64_t(c.j) * g.BS + c.c0) * TL::ROW_BYTES;
-  const char* kbase = kb + row_bytes;
-  const char* vbase = vb + row_bytes;
   const int last = c.nj - 1 - c.c0;  // last real key slot of the chunk
+  uint32_t row_off[TL::LOADS];       // byte offset of this lane's row in load qq
+  int64_t base_row;
+  auto fill = [&](auto row_of) {
+#pragma unroll
+    for (int qq = 0; qq < TL::LOADS; ++qq)
+      row_off[qq] = uint32_t(row_of(min(qq * TL::RPI + lane / TL::NCH, last)) * TL::ROW_BYTES);
+  };
+  if (!RASTER) {
+    base_row = head_row + int64_t(c.j) * g.BS + c.c0;
+    fill([](int sr) { return sr; });
+  } else {
+    const RasterRows rr = raster_rows(g, c, head_row);
+    base_row = rr.base;
+    if (rr.full)
+      fill([&](int sr) { return rel[c.c0 + sr]; });
+    else
+      fill([&](int sr) { return int(ext_token(g, c.e, c.c0 + sr)); });
+  }
+  const char* kbase = kb + base_row * TL::ROW_BYTES;
+  const char* vbase = vb + base_row * TL::ROW_BYTES;
 #pragma unroll
   for (int q = 0; q < 2 * TL::LOADS; ++q) {
     const bool is_v = q >= TL::LOADS;
     const int qq = is_v ? q - TL::LOADS : q;
     const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
     const int gp = (lane % TL::NCH) ^ (is_v ? swz_v(r) : swz_k<D>(r));
-    const uint32_t off = uint32_t(min(r, last) * TL::ROW_BYTES + gp * 16);
+    const uint32_t off = row_off[qq] + uint32_t(gp * 16);
     const uint32_t dst = lds_buf + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;  // M0
     asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(is_v ? vbase : kbase),
                  "{m0}"(dst)
@@ -142,7 +223,9 @@ __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, c
 // workgroup shapes are chosen so that a CU holds 12 waves at three waves per
 // SIMD (<= 168 VGPRs): 4 compute waves without a loader (3 workgroups per CU),
 // 5 compute waves with one (2 workgroups of 6).
-template <int D, int W, bool LD>
+// RASTER: q, k, v and o are raster [B,H,N,d] (and lse [B,H,N]); every row is
+// addressed through the blocking's slot -> token map, so no blocked copies exist.
+template <int D, int W, bool LD, bool RASTER>
 __global__ void __launch_bounds__(64 * (W + LD))
     __attribute__((amdgpu_waves_per_eu(W + LD >= 3 ? 3 : 2)))
     attn_kernel(DevGeom g, const uint4* __restrict__ qb, const char* __restrict__ kb,
@@ -151,9 +234,11 @@ __global__ void __launch_bounds__(64 * (W + LD))
                 float* __restrict__ lse) {
   using TL = Tile<D>;
   __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
+  __shared__ int rel_raw[RASTER ? kMaxBS : 1];  // full-block slot -> raster token offset
   extern __shared__ int list_raw[];  // kept list of this work item, NB entries
   lds_char* const lds = (lds_char*)lds_raw;
   lds_int* const list = (lds_int*)list_raw;
+  lds_int* const rel = (lds_int*)rel_raw;
 
   // Workgroup w runs on XCD w % 8. Every XCD walks the heads in the same order
   // and takes one contiguous eighth of each head's query blocks: the XCDs work
@@ -164,20 +249,25 @@ __global__ void __launch_bounds__(64 * (W + LD))
   const int64_t bh = slot / per_xcd;
   const int i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
   if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
-  const int n_i = block_ext(g, i).n;
+  const BlockExt e_i = block_ext(g, i);
+  const int n_i = e_i.n;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: keep in an SGPR
   const bool loader = LD && wave == W;  // loader wave: q0 = 32 W >= BS, so no query rows
   const int q0 = wave * 32;
   const int half = lane >> 5;  // k-slot group of the MFMA operands
   const int r32 = lane & 31;
-  const int64_t head_row = bh * g.NB * int64_t(g.BS);
+  const int64_t head_row = RASTER ? bh * g.N : bh * g.NB * int64_t(g.BS);
+  // row of query slot qs < n_i of this item
+  auto q_row = [&](int qs) -> int64_t {
+    return RASTER ? head_row + ext_token(g, e_i, qs) : head_row + int64_t(i) * g.BS + qs;
+  };
 
   // Q^T fragments (B operand): query row q0 + r32, d = 16*kk + 8*half .. +8
   bf16x8 qf[D / 16];
   {
     const int qs = q0 + r32;
-    const uint4* src = qb + (head_row + int64_t(i) * g.BS + qs) * TL::NCH + half;
+    const uint4* src = qb + q_row(min(qs, n_i - 1)) * TL::NCH + half;
 #pragma unroll
     for (int kk = 0; kk < D / 16; ++kk) {
       uint4 v = make_uint4(0, 0, 0, 0);
@@ -191,7 +281,13 @@ __global__ void __launch_bounds__(64 * (W + LD))
     const int* src = indices + (bh * g.NB + i) * int64_t(g.NB);
     for (int e = threadIdx.x; e < cnt; e += 64 * (W + LD)) list[e] = src[e];
   }
-  __syncthreads();  // list visible to every wave (also completes the Q loads)
+  if (RASTER) {
+    for (int sl = threadIdx.x; sl < g.BS; sl += 64 * (W + LD)) {
+      const int q = sl / g.bw;
+      rel[sl] = ((q / g.bh) * g.Hs + q % g.bh) * g.Ws + sl % g.bw;
+    }
+  }
+  __syncthreads();  // list and table visible to every wave (also completes the Q loads)
 
   // per-lane LDS byte offsets that do not depend on the chunk
   // K operand: tile row r32, global piece 2*kk + half
@@ -213,24 +309,47 @@ __global__ void __launch_bounds__(64 * (W + LD))
   const bf16x2 ones = {__bf16(1.0f), __bf16(1.0f)};
 
   const uint32_t lds_u32 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  int rows[WaveLoads<D, W>::NQ];  // without a loader: this wave's rows of the next chunk
   // issue the loads of chunk c into buffer b (all of them from the loader wave,
-  // or each wave its share)
+  // or each wave its share at the rows prefetched into `rows`)
   auto issue = [&](const Cursor& c, int b) {
     if (LD) {
-      if (loader) loader_chunk<D>(g, kb, vb, head_row, c, lds_u32 + b * TL::BUF_BYTES, lane);
+      if (loader)
+        loader_chunk<D, RASTER>(g, kb, vb, head_row, c, rel, lds_u32 + b * TL::BUF_BYTES, lane);
     } else {
-      load_chunk<D, W>(g, kb, vb, head_row, c, lds + b * TL::BUF_BYTES, wave, lane);
+      load_chunk<D, W, RASTER>(g, kb, vb, head_row, c, rows, lds + b * TL::BUF_BYTES, wave, lane);
     }
   };
-  Cursor cur = {-1, 0, 0, -kChunk};
+  auto prefetch = [&](const Cursor& c) {
+    if (!LD) wave_rows<D, W, RASTER>(g, c, rel, wave, lane, rows);
+  };
+  Cursor cur = {-1, 0, 0, -kChunk, e_i};
   cur = next_chunk(g, list, cnt, cur);
   int buf = 0;
-  if (cur.jj < cnt) issue(cur, 0);
+  if (cur.jj < cnt) {
+    prefetch(cur);
+    issue(cur, 0);
+  }
+  Cursor ahead = cur;  // without a loader: the chunk after the next, rows prefetched
+  if (!LD) {
+    ahead = next_chunk(g, list, cnt, cur);
+    if (ahead.jj < cnt) prefetch(ahead);
+  }
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   while (cur.jj < cnt) {
-    const Cursor nxt = next_chunk(g, list, cnt, cur);
-    if (nxt.jj < cnt) issue(nxt, buf ^ 1);
+    Cursor nxt;
+    if (LD) {
+      nxt = next_chunk(g, list, cnt, cur);
+      if (nxt.jj < cnt) issue(nxt, buf ^ 1);
+    } else {
+      nxt = ahead;
+      if (nxt.jj < cnt) {
+        issue(nxt, buf ^ 1);
+        ahead = next_chunk(g, list, cnt, nxt);
+        if (ahead.jj < cnt) prefetch(ahead);
+      }
+    }
     if (rows_live) {
       lds_char* Kt = lds + buf * TL::BUF_BYTES;
       lds_char* Vt = Kt + TL::TILE_BYTES;
@@ -332,10 +451,12 @@ __global__ void __launch_bounds__(64 * (W + LD))
     l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
   }
   const int qs = q0 + r32;
-  if (qs < g.BS) {
+  // blocked output: every slot of the block (padding as zeros); raster: real rows only
+  if (RASTER ? qs < n_i : qs < g.BS) {
     const bool real = qs < n_i;
     const float inv = (real && l > 0.0f) ? 1.0f / l : 0.0f;
-    __bf16* dst = ob + (head_row + int64_t(i) * g.BS + qs) * D + 4 * half;
+    const int64_t orow = real ? q_row(qs) : head_row + int64_t(i) * g.BS + qs;
+    __bf16* dst = ob + orow * D + 4 * half;
 #pragma unroll
     for (int t = 0; t < D / 32; ++t)
 #pragma unroll
@@ -346,45 +467,43 @@ __global__ void __launch_bounds__(64 * (W + LD))
         *reinterpret_cast<bf16x4*>(dst + 32 * t + 8 * rq) = v;
       }
     if (lse && real && half == 0)
-      lse[head_row + int64_t(i) * g.BS + qs] =
-          l > 0.0f ? (m + log2f(l)) * 0.69314718055994530942f : -INFINITY;
+      lse[orow] = l > 0.0f ? (m + log2f(l)) * 0.69314718055994530942f : -INFINITY;
   }
 }
 
-template <int D, int W, bool LD>
+template <int D, int W, bool LD, bool RASTER>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                      hipStream_t s) {
   const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
   static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W, LD>),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W, LD, RASTER>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        int(kMaxAttnNB * sizeof(int)));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  attn_kernel<D, W, LD><<<dim3(unsigned(items)), 64 * (W + LD), size_t(g.NB) * sizeof(int), s>>>(
+  attn_kernel<D, W, LD, RASTER><<<dim3(unsigned(items)), 64 * (W + LD), size_t(g.NB) * sizeof(int),
+                                  s>>>(
       g, static_cast<const uint4*>(qb), static_cast<const char*>(kb),
       static_cast<const char*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
   return hipGetLastError();
 }
 
-template <int D>
+template <int D, bool RASTER>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                     hipStream_t s) {
+#define SPADE_ATTN_CASE(w, ld) \
+  case w: return launch_dw<D, w, ld, RASTER>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
   // loader wave unless it would cost a workgroup per CU (4 or 6 compute waves)
   switch ((g.BS + 31) / 32) {
-    case 1: return launch_dw<D, 1, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 2: return launch_dw<D, 2, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 3: return launch_dw<D, 3, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 4: return launch_dw<D, 4, false>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 5: return launch_dw<D, 5, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 6: return launch_dw<D, 6, false>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 7: return launch_dw<D, 7, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-    case 8: return launch_dw<D, 8, true>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+    SPADE_ATTN_CASE(1, true) SPADE_ATTN_CASE(2, true) SPADE_ATTN_CASE(3, true)
+    SPADE_ATTN_CASE(4, false) SPADE_ATTN_CASE(5, true) SPADE_ATTN_CASE(6, false)
+    SPADE_ATTN_CASE(7, true) SPADE_ATTN_CASE(8, true)
   }
+#undef SPADE_ATTN_CASE
   return hipErrorInvalidValue;
 }
 
@@ -394,10 +513,15 @@ size_t attn_workspace_bytes(const DevGeom&) { return 0; }
 
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,
-                                    float scale, void* ob, float* lse, void*, hipStream_t s) {
-  const float scale_log2 = scale * 1.44269504088896340736f;
-  if (g.d == 128) return launch_d<128>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
-  if (g.d == 64) return launch_d<64>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+                                    float scale, void* ob, float* lse, void*, bool raster,
+                                    hipStream_t s) {
+  const float sl2 = scale * 1.44269504088896340736f;
+  if (g.d == 128)
+    return raster ? launch_d<128, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s)
+                  : launch_d<128, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s);
+  if (g.d == 64)
+    return raster ? launch_d<64, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s)
+                  : launch_d<64, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s);
   return hipErrorInvalidValue;
 }
 

@@ -49,8 +49,10 @@ struct HeadMap {
 };
 
 // Raster token of slot `slot` of block e: slots follow raster order of (dt, dy, dx).
-// r_ew = 1/e.ew and r_eh = 1/e.eh; the float quotients are exact because slots and
-// extents stay below 2^8 (see kMaxBS).
+// r_ew and r_eh are 1/e.ew and 1/e.eh to within a few ulp (a division or
+// v_rcp_f32): slots and extents stay below 2^8 (see kMaxBS), so (slot + 0.5) / ew
+// lies at least 2^-9 from an integer, far beyond the float error, and the
+// truncation yields the exact quotient.
 __device__ __forceinline__ int64_t block_slot_token(const DevGeom& g, const BlockExt& e,
                                                    float r_ew, float r_eh, int slot) {
   const int q = int((float(slot) + 0.5f) * r_ew);  // slot / ew
@@ -88,7 +90,7 @@ hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const do
 size_t attn_workspace_bytes(const DevGeom& g);
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,
-                                    float scale, void* ob, float* lse, void* ws,
+                                    float scale, void* ob, float* lse, void* ws, bool raster,
                                     hipStream_t s);
 
 constexpr int kMaxBS = 256;        // attention: one wave per 32 query rows, <= 8 waves

@@ -3,9 +3,12 @@
 blocking (Q, K, V) -> summaries -> estimate + select -> block-sparse attention
 -> restore layout. By default the blocking of Q and K and their summaries are
 one fused call (spade_block_summarize, §3.3 optimisation (1)); `fused=False`
-issues spade_block_reorder x3 + spade_summarize instead. All buffers are
-allocated once here (torch, device memory); `run` only issues the library calls
-on one stream, with no host sync.
+issues spade_block_reorder x3 + spade_summarize instead. With `virtual=True`
+nothing is copied into the blocked layout: the summaries are read straight from
+the raster Q, K and the attention gathers its rows from, and writes O back to,
+the raster tensors (spade_sparse_attn_raster). All buffers are allocated once
+here (torch, device memory); `run` only issues the library calls on one stream,
+with no host sync.
 """
 from __future__ import annotations
 
@@ -28,9 +31,12 @@ def block_valid_counts(g) -> np.ndarray:
 
 class SpadePath:
     def __init__(self, B, H, d, T, Hs, Ws, bt, bh, bw, *, mode="topp", topk=None, tau=None,
-                 scale=None, device="cuda", with_sics=False, with_lse=False, fused=True):
+                 scale=None, device="cuda", with_sics=False, with_lse=False, fused=True,
+                 virtual=False):
         self.g = S.geom(B, H, d, T, Hs, Ws, bt, bh, bw)
-        self.fused = bool(fused)
+        self.virtual = bool(virtual)
+        self.fused = bool(fused) or self.virtual
+        self._qkv = None
         self.mode = S.SPADE_TOPP if mode == "topp" else S.SPADE_TOPK
         self.topk = int(topk or 0)
         self.tau = float(tau if tau is not None else 1.0)
@@ -38,7 +44,8 @@ class SpadePath:
         g, dev = self.g, device
         NB, BS = g.NB, g.BS
         bf = torch.bfloat16
-        self.Qb = torch.empty((B, H, NB * BS, d), dtype=bf, device=dev)
+        blocked = (0,) if self.virtual else (B, H, NB * BS, d)
+        self.Qb = torch.empty(blocked, dtype=bf, device=dev)
         self.Kb = torch.empty_like(self.Qb)
         self.Vb = torch.empty_like(self.Qb)
         self.Ob = torch.empty_like(self.Qb)
@@ -49,13 +56,20 @@ class SpadePath:
         self.sics_k = torch.empty_like(self.sics_q) if with_sics else None
         self.counts = torch.empty((B, H, NB), dtype=torch.int32, device=dev)
         self.indices = torch.empty((B, H, NB, NB), dtype=torch.int32, device=dev)
-        self.lse = torch.empty((B, H, NB * BS), dtype=torch.float32, device=dev) if with_lse else None
+        lse_rows = g.N if self.virtual else NB * BS
+        self.lse = torch.empty((B, H, lse_rows), dtype=torch.float32, device=dev) if with_lse else None
         nws = S.spade_attn_workspace_bytes(g)
         self.ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
 
     # individual stages, so they can be timed separately
     def reorder_in(self, Q, K, V, stream=None):
-        """Blocking of Q, K, V; in fused mode also the summaries of Q and K."""
+        """Blocking of Q, K, V; in fused mode also the summaries of Q and K; in
+        virtual mode only the summaries (the raster tensors are kept for attend)."""
+        if self.virtual:
+            S.spade_block_summarize(self.g, Q, K, qbar=self.qbar, kbar=self.kbar,
+                                    sics_q=self.sics_q, sics_k=self.sics_k, stream=stream)
+            self._qkv = (Q, K, V)
+            return
         if self.fused:
             S.spade_block_summarize(self.g, Q, K, self.Qb, self.Kb, self.qbar, self.kbar,
                                     self.sics_q, self.sics_k, stream=stream)
@@ -76,12 +90,21 @@ class SpadePath:
                                 self.scale, self.counts, self.indices, stream=stream)
 
     def attend(self, counts=None, indices=None, stream=None):
+        if self.virtual:
+            Q, K, V = self._qkv
+            S.spade_sparse_attn_raster(self.g, Q, K, V,
+                                       self.counts if counts is None else counts,
+                                       self.indices if indices is None else indices,
+                                       self.scale, self.O, self.lse, self.ws, stream=stream)
+            return
         S.spade_block_sparse_attn(self.g, self.Qb, self.Kb, self.Vb,
                                   self.counts if counts is None else counts,
                                   self.indices if indices is None else indices,
                                   self.scale, self.Ob, self.lse, self.ws, stream=stream)
 
     def restore(self, stream=None):
+        if self.virtual:  # the attention already wrote O in raster order
+            return
         S.spade_block_reorder(self.g, self.Ob, self.O, inverse=True, stream=stream)
 
     def run(self, Q, K, V, stream=None):

@@ -21,7 +21,8 @@ SPADE_TOPK, SPADE_TOPP = 0, 1
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_attn_workspace_bytes",
-            "spade_block_sparse_attn", "spade_status_string", "spade_last_error")
+            "spade_block_sparse_attn", "spade_sparse_attn_raster", "spade_status_string",
+            "spade_last_error")
 MAX_HEAD_LIST = 64
 
 
@@ -74,6 +75,7 @@ def lib() -> ctypes.CDLL:
             "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
+            "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_status_string": (ctypes.c_char_p, [i32]),
             "spade_last_error": (ctypes.c_char_p, []),
         }
@@ -158,3 +160,11 @@ def spade_block_sparse_attn(g: spade_geom, qb, kb, vb, counts, indices, scale: f
     _check(lib().spade_block_sparse_attn(ctypes.byref(g), _p(qb), _p(kb), _p(vb), _p(counts),
                                          _p(indices), float(scale), _p(ob), _p(lse),
                                          _p(workspace), nbytes, _s(stream)))
+
+
+def spade_sparse_attn_raster(g: spade_geom, q, k, v, counts, indices, scale: float, o, lse=None,
+                             workspace=None, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spade_sparse_attn_raster(ctypes.byref(g), _p(q), _p(k), _p(v), _p(counts),
+                                          _p(indices), float(scale), _p(o), _p(lse),
+                                          _p(workspace), nbytes, _s(stream)))

@@ -33,13 +33,18 @@ def _case(name):
         "bs256_max": dict(T=8, Hs=16, Ws=12, bt=4, bh=8, bw=8, d=128, H=1),    # BS 256: 8 waves
         "one_token": dict(T=1, Hs=1, Ws=1, bt=1, bh=1, bw=1, d=64, H=2),       # NB = BS = N = 1
         "one_block": dict(T=3, Hs=5, Ws=7, bt=4, bh=8, bw=8, d=128, H=2),      # a single padded block
+        # workgroups without a loader wave (4 or 6 compute waves), ragged on every axis
+        "w4_ragged": dict(T=7, Hs=12, Ws=21, bt=3, bh=5, bw=8, d=128, H=2),    # BS 120
+        "w4_ragged_d64": dict(T=9, Hs=11, Ws=12, bt=4, bh=5, bw=5, d=64, H=2),  # BS 100
+        "w6_ragged": dict(T=7, Hs=13, Ws=23, bt=3, bh=6, bw=10, d=128, H=2),   # BS 180
     }
     kw = dict(table[name])
     return P.small_cfg(kw.pop("T"), kw.pop("Hs"), kw.pop("Ws"), kw.pop("bt"), kw.pop("bh"),
                        kw.pop("bw"), **kw)
 
 
-SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block"]
+SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block",
+         "w4_ragged", "w4_ragged_d64", "w6_ragged"]
 
 
 def _say(*a):
