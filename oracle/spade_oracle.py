@@ -39,6 +39,31 @@ design notes):
     batch mean; the first candidate with the highest score wins;
   * the block-shape sweep keeps k = max(1, round((1 - s) NB)) blocks per row
     for a target block sparsity s.
+Readings of the full mask composition (§3.1 vDiT-SSR, §3.3; the figure that
+defines the DSA estimators is not part of the text, so those two are readings
+that no printed value pins — "parity unpinned" with respect to the paper; the
+tests pin them to the bounds they are built to be):
+  * max/min Summarizer: elementwise max and min over each block's real tokens;
+  * DSA estimate: with q~ = (q_max + q_min) / 2, scale * sum_c max(q~_c k_max_c,
+    q~_c k_min_c), the largest <q~, k> over the box spanned by block j's keys;
+  * DSA2 estimate: scale * sum_c of the largest of the four products of
+    {q_max_c, q_min_c} and {k_max_c, k_min_c}: the largest <q, k> over both
+    blocks' boxes, so it bounds every logit of the block pair from above;
+  * intra-block filter (the intra-top value): a block's coherence is
+    SICS / n_b^2 (the mean pairwise cosine similarity, self pairs included);
+    the filter marks incoherent blocks, whose summary is least trustworthy:
+    coherence < theta (threshold mode) or the k least coherent blocks of the
+    head (Top-K mode, ties to the lower index). A marked Q block keeps its whole
+    row and a marked K block its whole column (intra scores broadcast and
+    OR-combined with the inter selection);
+  * local window (w_t, w_h, w_w) in block units: key block j is kept for query
+    block i when their block-grid coordinates differ by at most w on each axis;
+    a negative radius disables the window;
+  * attention sink of s tokens: every query block keeps the key blocks holding
+    any of the first s raster tokens;
+  * the mask is the OR of the inter Top-K/Top-P selection (computed on the inter
+    scores alone) and the parts above; per-head k or tau values (the policy's
+    head-wise budgets) replace the scalar ones.
 
 Every array here is float64 (inputs are upcast first). Shapes: Q, K, V are
 [B, H, N, d]; blocked tensors are [B, H, NB*BS, d].
@@ -414,6 +439,197 @@ def block_sparse_attention(Qb, Kb, Vb, counts, indices, g: Geometry, scale: floa
         Ob[b, h, i * BS: i * BS + n_valid[i]] = (w @ vs) / z
         lse[b, h, i * BS: i * BS + n_valid[i]] = (mx + np.log(z))[:, 0]
     return Ob, lse
+
+
+# --------------------------------------------------------------------------
+# Max/min Summarizer and the DSA / DSA2 inter-estimators (§3.1 Summarizer and
+# Estimator Expressions; DSA-SPADE is the variant the experiments run, §4)
+# --------------------------------------------------------------------------
+def block_maxmin(Xb: np.ndarray, g: Geometry):
+    """[B, H, NB*BS, d] -> (max, min), each [B, H, NB, d], over valid slots only."""
+    _, n_valid = block_tables(g)
+    Xb = np.asarray(Xb, dtype=np.float64)
+    shape = Xb.shape[:-2] + (g.NB, Xb.shape[-1])
+    mx, mn = np.empty(shape), np.empty(shape)
+    for b in range(g.NB):
+        rows = Xb[..., b * g.BS: b * g.BS + n_valid[b], :]
+        mx[..., b, :] = rows.max(axis=-2)
+        mn[..., b, :] = rows.min(axis=-2)
+    return mx, mn
+
+
+def dsa_scores(qmax, qmin, kmax, kmin, scale: float) -> np.ndarray:
+    """DSA estimate [.., NB, NB]: per channel the larger of q~*k_max and q~*k_min,
+    summed over channels, with q~ the midpoint of the query block's range."""
+    qt = (qmax + qmin) / 2.0
+    out = np.empty(qt.shape[:-1] + (kmax.shape[-2],))
+    for i in range(qt.shape[-2]):
+        a = qt[..., i:i + 1, :]
+        out[..., i, :] = np.maximum(a * kmax, a * kmin).sum(axis=-1)
+    return out * scale
+
+
+def dsa2_scores(qmax, qmin, kmax, kmin, scale: float) -> np.ndarray:
+    """DSA2 estimate [.., NB, NB]: per channel the largest product of a query
+    extreme and a key extreme, summed over channels."""
+    out = np.empty(qmax.shape[:-1] + (kmax.shape[-2],))
+    for i in range(qmax.shape[-2]):
+        hi, lo = qmax[..., i:i + 1, :], qmin[..., i:i + 1, :]
+        corners = np.stack([hi * kmax, hi * kmin, lo * kmax, lo * kmin])
+        out[..., i, :] = corners.max(axis=0).sum(axis=-1)
+    return out * scale
+
+
+# --------------------------------------------------------------------------
+# Intra-block filter, local window, attention sink and their composition with
+# the inter selection (§3.1 sparsity-ratio scheme and utility parameters; §3.3:
+# intra scores broadcast and OR-combined with the inter scores, the result
+# united with the local-window and attention-sink masks)
+# --------------------------------------------------------------------------
+def block_coherence(sics: np.ndarray, g: Geometry) -> np.ndarray:
+    """SICS / n_b^2 per block: 1 when every vector of the block is parallel."""
+    _, n_valid = block_tables(g)
+    return np.asarray(sics, dtype=np.float64) / (n_valid.astype(np.float64) ** 2)
+
+
+def intra_marks(sics: np.ndarray, g: Geometry, mode: str, theta=None, k=None) -> np.ndarray:
+    """Boolean [.., NB]: the blocks the intra-block filter marks (incoherent ones)."""
+    c = block_coherence(sics, g)
+    if mode == "threshold":
+        return c < theta
+    assert mode == "topk"
+    marks = np.zeros(c.shape, dtype=bool)
+    j = np.arange(c.shape[-1])
+    for idx in np.ndindex(*c.shape[:-1]):
+        order = np.lexsort((j, c[idx]))          # coherence ascending, index ascending
+        marks[idx + (order[: min(k, c.shape[-1])],)] = True
+    return marks
+
+
+def block_coords(g: Geometry) -> np.ndarray:
+    """[NB, 3] block-grid coordinates (tb, hb, wb) of every block, T-major order."""
+    nT, nH, nW = g.grid
+    return np.array([(tb, hb, wb) for tb in range(nT) for hb in range(nH) for wb in range(nW)],
+                    dtype=np.int64)
+
+
+def window_mask(g: Geometry, w) -> np.ndarray:
+    """[NB, NB]: key block j within the (w_t, w_h, w_w) block window of query block i."""
+    if w is None or min(w) < 0:
+        return np.zeros((g.NB, g.NB), dtype=bool)
+    c = block_coords(g)
+    diff = np.abs(c[:, None, :] - c[None, :, :])
+    return np.all(diff <= np.asarray(w, dtype=np.int64), axis=-1)
+
+
+def sink_blocks(g: Geometry, s: int) -> np.ndarray:
+    """[NB]: blocks holding at least one of the first s raster tokens."""
+    slot_token, n_valid = block_tables(g)
+    marks = np.zeros(g.NB, dtype=bool)
+    for b in range(g.NB):
+        toks = slot_token[b * g.BS: b * g.BS + n_valid[b]]
+        marks[b] = bool(np.any(toks < s))
+    return marks
+
+
+@dataclass(frozen=True)
+class MaskSpec:
+    """What one selection call composes (§3.1 sparsity-ratio scheme)."""
+    estimator: str = "mean"            # "mean" | "dsa" | "dsa2"
+    mode: str = "topk"                 # inter rule: "topk" | "topp"
+    topk: int | None = None
+    tau: float | None = None
+    topk_per_head: tuple | None = None  # [H] budgets replacing topk
+    tau_per_head: tuple | None = None   # [H] budgets replacing tau
+    intra: str | None = None           # None | "threshold" | "topk"
+    intra_theta: float | None = None
+    intra_topk: int | None = None
+    window: tuple | None = None        # (w_t, w_h, w_w) block radii
+    sink: int = 0                      # attention-sink length in tokens
+
+
+def select_per_head(scores: np.ndarray, spec: MaskSpec):
+    """The inter rule on [B, H, NB, NB] scores, with per-head k or tau if given."""
+    H = scores.shape[1]
+    counts = np.zeros(scores.shape[:-1], dtype=np.int32)
+    indices = np.full(scores.shape, -1, dtype=np.int32)
+    for h in range(H):
+        k = spec.topk_per_head[h] if spec.topk_per_head is not None else spec.topk
+        t = spec.tau_per_head[h] if spec.tau_per_head is not None else spec.tau
+        c, ix = select(scores[:, h:h + 1], spec.mode, topk=k, tau=t)
+        counts[:, h:h + 1], indices[:, h:h + 1] = c, ix
+    return counts, indices
+
+
+def compose_mask(inter: np.ndarray, intra_q=None, intra_k=None, window=None, sink=None):
+    """[B, H, NB, NB] OR of the inter mask, the broadcast intra marks (rows for
+    Q, columns for K), the window [NB, NB] and the sink columns [NB]."""
+    m = inter.copy()
+    if intra_q is not None:
+        m |= intra_q[..., :, None]
+    if intra_k is not None:
+        m |= intra_k[..., None, :]
+    if window is not None:
+        m |= window
+    if sink is not None:
+        m |= sink
+    return m
+
+
+def lists_from_mask(mask: np.ndarray):
+    """counts [.., NB] and ascending index lists [.., NB, NB] (-1 padded) of a mask."""
+    NB = mask.shape[-1]
+    counts = mask.sum(axis=-1).astype(np.int32)
+    indices = np.full(mask.shape, -1, dtype=np.int32)
+    for idx in np.ndindex(*mask.shape[:-1]):
+        kept = np.nonzero(mask[idx])[0]
+        indices[idx + (slice(0, kept.size),)] = kept
+    assert indices.shape[-1] == NB
+    return counts, indices
+
+
+def composed_selection(Q, K, g: Geometry, spec: MaskSpec, scale=None) -> dict:
+    """Blocking -> Summarizer -> estimator -> inter rule -> intra filter, window
+    and sink -> OR -> block lists (§3.3 order)."""
+    Q, K = (np.asarray(a, dtype=np.float64) for a in (Q, K))
+    scale = 1.0 / np.sqrt(Q.shape[-1]) if scale is None else scale
+    Qb, Kb = reorder(Q, g), reorder(K, g)
+    out = {}
+    if spec.estimator == "mean":
+        qbar, kbar = block_means(Qb, g), block_means(Kb, g)
+        s = block_scores(qbar, kbar, scale)
+        out.update(qbar=qbar, kbar=kbar)
+    else:
+        (qmax, qmin), (kmax, kmin) = block_maxmin(Qb, g), block_maxmin(Kb, g)
+        est = dsa_scores if spec.estimator == "dsa" else dsa2_scores
+        s = est(qmax, qmin, kmax, kmin, scale)
+        out.update(qmax=qmax, qmin=qmin, kmax=kmax, kmin=kmin)
+    ci, ii = select_per_head(s, spec)
+    inter = block_mask(ci, ii)
+    iq = ik = None
+    if spec.intra is not None:
+        sq, sk = block_sics(Qb, g), block_sics(Kb, g)
+        iq = intra_marks(sq, g, spec.intra, spec.intra_theta, spec.intra_topk)
+        ik = intra_marks(sk, g, spec.intra, spec.intra_theta, spec.intra_topk)
+        out.update(sics_q=sq, sics_k=sk)
+    win = window_mask(g, spec.window) if spec.window is not None else None
+    snk = sink_blocks(g, spec.sink) if spec.sink > 0 else None
+    mask = compose_mask(inter, iq, ik, win, snk)
+    counts, indices = lists_from_mask(mask)
+    out.update(scores=s, inter_counts=ci, inter_indices=ii, intra_q=iq, intra_k=ik,
+               mask=mask, counts=counts, indices=indices, Qb=Qb, Kb=Kb)
+    return out
+
+
+def spade_attention_composed(Q, K, V, g: Geometry, spec: MaskSpec, scale=None) -> dict:
+    """The whole path with the composed mask: selection, Eq. (2), restore."""
+    V = np.asarray(V, dtype=np.float64)
+    scale = 1.0 / np.sqrt(V.shape[-1]) if scale is None else scale
+    r = composed_selection(Q, K, g, spec, scale)
+    Ob, lse = block_sparse_attention(r["Qb"], r["Kb"], reorder(V, g), r["counts"],
+                                     r["indices"], g, scale)
+    r.update(O=inverse_reorder(Ob, g), Ob=Ob, lse=lse)
+    return r
 
 
 # --------------------------------------------------------------------------

@@ -143,3 +143,59 @@ def test_group_output_in_wrong_heads_is_caught(monkeypatch):
     monkeypatch.setattr(O, "spade_attention", shifted)
     assert _fails(TW.test_sweep_outputs_land_in_their_heads) or _fails(
         TW.test_sweep_keeping_every_block_is_dense_attention)
+
+
+# ---- full mask composition ----
+from . import test_oracle_mask as TK  # noqa: E402
+
+
+def test_dsa_taking_the_smaller_product_is_caught(monkeypatch):
+    def dsa_min(qmax, qmin, kmax, kmin, scale):
+        qt = (qmax + qmin) / 2.0
+        out = np.empty(qt.shape[:-1] + (kmax.shape[-2],))
+        for i in range(qt.shape[-2]):
+            a = qt[..., i:i + 1, :]
+            out[..., i, :] = np.minimum(a * kmax, a * kmin).sum(axis=-1)
+        return out * scale
+    monkeypatch.setattr(O, "dsa_scores", dsa_min)
+    assert _fails(TK.test_dsa_bounds_every_key_and_is_reached_at_a_corner)
+
+
+def test_dsa2_missing_a_corner_is_caught(monkeypatch):
+    def three_corners(qmax, qmin, kmax, kmin, scale):
+        out = np.empty(qmax.shape[:-1] + (kmax.shape[-2],))
+        for i in range(qmax.shape[-2]):
+            hi, lo = qmax[..., i:i + 1, :], qmin[..., i:i + 1, :]
+            out[..., i, :] = np.stack([hi * kmax, hi * kmin, lo * kmax]).max(axis=0).sum(axis=-1)
+        return out * scale
+    monkeypatch.setattr(O, "dsa2_scores", three_corners)
+    assert _fails(TK.test_dsa2_bounds_every_logit_of_the_pair)
+
+
+def test_window_radius_off_by_one_is_caught(monkeypatch):
+    def strict(g, w):
+        if w is None or min(w) < 0:
+            return np.zeros((g.NB, g.NB), dtype=bool)
+        c = O.block_coords(g)
+        return np.all(np.abs(c[:, None, :] - c[None, :, :]) < np.asarray(w) + 0, axis=-1)
+    monkeypatch.setattr(O, "window_mask", strict)
+    assert _fails(TK.test_window_row_counts_closed_form, (1, 1, 1))
+
+
+def test_sink_counted_in_blocks_is_caught(monkeypatch):
+    monkeypatch.setattr(O, "sink_blocks", lambda g, s: np.arange(g.NB) < s)
+    assert _fails(TK.test_sink_blocks_by_token_count)
+
+
+def test_intra_marking_the_most_coherent_is_caught(monkeypatch):
+    orig = O.block_coherence
+    monkeypatch.setattr(O, "block_coherence", lambda sics, g: -orig(sics, g))
+    assert _fails(TK.test_intra_topk_table_by_hand)
+
+
+def test_key_marks_broadcast_along_rows_is_caught(monkeypatch):
+    orig = O.compose_mask
+    monkeypatch.setattr(O, "compose_mask",
+                        lambda inter, iq=None, ik=None, w=None, s=None:
+                        orig(inter, iq, None, w, s) | (ik[..., :, None] if ik is not None else False))
+    assert _fails(TK.test_composition_is_the_or_of_its_parts)
