@@ -10,6 +10,11 @@
  *   spade_block_summarize    the two above fused into one pass over the raster
  *                            tensors (§3.3 (1)), optionally for a group of heads
  *   spade_estimate_select    inter-block Estimator + Top-K / Top-P index search
+ *   spade_block_minmax       max/min Summarizer + optional SICS, from the raster
+ *                            tensors (the summaries of the DSA estimators)
+ *   spade_compose_select     the full mask: an estimator (mean, DSA, DSA2), the
+ *                            Top-K/Top-P rule with optional per-head budgets, the
+ *                            intra-block filter, local window and attention sink
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
@@ -62,6 +67,8 @@ typedef enum {
 
 enum { SPADE_BF16 = 0, SPADE_FP32 = 1 };  /* element type of spade_block_reorder */
 enum { SPADE_TOPK = 0, SPADE_TOPP = 1 };  /* row rule of spade_estimate_select   */
+enum { SPADE_EST_MEAN = 0, SPADE_EST_DSA = 1, SPADE_EST_DSA2 = 2 };  /* inter-block estimator */
+enum { SPADE_INTRA_NONE = 0, SPADE_INTRA_THRESHOLD = 1, SPADE_INTRA_TOPK = 2 };  /* intra filter */
 
 /* Problem geometry: batch, heads, head dim; latent grid; blocking scheme. */
 typedef struct {
@@ -185,6 +192,89 @@ spade_status spade_estimate_select(const spade_geom* g, const double* qbar, cons
                                    int32_t mode, int32_t topk, double tau, double scale,
                                    int32_t* counts, int32_t* indices, double* scores,
                                    hipStream_t stream);
+
+/*
+ * Max/min Summarizer and intra-block estimator from the raster tensors — paper
+ * §3.1 (the Summarizer Expression reduces over a block's positions with max, min
+ * or mean; the DSA-SPADE and DSA2-SPADE estimators take the max and min
+ * summaries) and §3.2 (SICS), in one pass over each block's rows (§3.3 (1)).
+ *
+ *   q, k:         raster bf16 [B,H,N,d].
+ *   qmax, qmin, kmax, kmin: out, fp64 [B,n,NB,d]: elementwise max / min over each
+ *                 block's real tokens (exact).
+ *   sics_q, sics_k: out, nullable (both or neither), fp64 [B,n,NB]: SICS, bit-equal
+ *                 to spade_block_summarize's.
+ *   heads, n_heads: head list as in spade_block_reorder; n = n_heads (H if NULL).
+ */
+spade_status spade_block_minmax(const spade_geom* g, const void* q, const void* k, double* qmax,
+                                double* qmin, double* kmax, double* kmin, double* sics_q,
+                                double* sics_k, const int32_t* heads, int32_t n_heads,
+                                hipStream_t stream);
+
+/* Block summaries a selection call reads (device pointers, fp64, [B,H,NB,d] or
+ * [B,H,NB] for SICS); each estimator and filter names the fields it needs. */
+typedef struct {
+  const double* qbar;   /* SPADE_EST_MEAN: block means of Q and K */
+  const double* kbar;
+  const double* qmax;   /* SPADE_EST_DSA, SPADE_EST_DSA2: block max / min */
+  const double* qmin;
+  const double* kmax;
+  const double* kmin;
+  const double* sics_q; /* intra-block filter: SICS of the Q and K blocks */
+  const double* sics_k;
+} spade_summaries;
+
+/* One head-wise sparsity scheme (paper §3.1: estimator expression, Top-K/Top-P
+ * inter value, intra value, local-window length, attention-sink length). Host
+ * struct, read before the call returns; the per-head arrays are device memory. */
+typedef struct {
+  int32_t estimator;     /* SPADE_EST_MEAN | SPADE_EST_DSA | SPADE_EST_DSA2 */
+  int32_t mode;          /* inter rule: SPADE_TOPK | SPADE_TOPP */
+  int32_t topk;          /* SPADE_TOPK: blocks per row (>= 1 unless topk_per_head) */
+  double tau;            /* SPADE_TOPP: mass in (0, 1] (unless tau_per_head) */
+  double scale;          /* logit scale of the estimate, normally 1/sqrt(d) */
+  const int32_t* topk_per_head; /* nullable DEVICE int32 [H]: replaces topk, each
+                                   value clamped to [1, NB] */
+  const double* tau_per_head;   /* nullable DEVICE fp64 [H]: replaces tau; >= 1 keeps
+                                   every block, <= 0 or NaN keeps the top block */
+  int32_t intra;         /* SPADE_INTRA_NONE | _THRESHOLD | _TOPK */
+  int32_t intra_topk;    /* _TOPK: how many least coherent blocks per head (>= 0) */
+  double intra_theta;    /* _THRESHOLD: coherence bound */
+  int32_t window[3];     /* local window radii in blocks along (t, y, x); any
+                            negative radius: no window */
+  int64_t sink_tokens;   /* attention-sink length in raster tokens (>= 0) */
+} spade_mask_spec;
+
+/*
+ * Full mask composition — paper §3.3: the inter-block importance matrix from the
+ * Estimator Expression, filtered by Top-K or Top-P; intra-block scores
+ * broadcast and OR-combined with it; the result united with the local-window
+ * and attention-sink masks; §3.1: the sparsity-ratio scheme's parts, and
+ * head-wise budgets (the policy function's output per head).
+ *
+ *   Estimate, fp64, times scale:
+ *     MEAN: <qbar_i, kbar_j>;
+ *     DSA:  sum_c max(m_c kmax_jc, m_c kmin_jc) with m = (qmax_i + qmin_i)/2, the
+ *           largest <m, k> over the box spanned by block j's keys;
+ *     DSA2: sum_c of the largest product of {qmax_ic, qmin_ic} and
+ *           {kmax_jc, kmin_jc}: an upper bound of every logit of the block pair.
+ *   Inter rule per row as in spade_estimate_select (the head's per-head k or tau
+ *   when given).
+ *   Block j is kept in row i when the inter rule keeps it, or
+ *     - the intra filter marks query block i (its whole row is kept) or key
+ *       block j (its whole column). A block's coherence is SICS / n_b^2; the
+ *       filter marks coherence < intra_theta (_THRESHOLD) or the intra_topk least
+ *       coherent blocks of the head, ties to the lower index (_TOPK);
+ *     - the block-grid coordinates of i and j differ by at most window[] on
+ *       every axis;
+ *     - block j holds one of the first sink_tokens raster tokens.
+ *   counts, indices, scores: as in spade_estimate_select (scores = the estimate).
+ *   Requires NB <= 1024. With everything but the inter rule off and the MEAN
+ *   estimator the result equals spade_estimate_select's.
+ */
+spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* spec,
+                                  const spade_summaries* sum, int32_t* counts, int32_t* indices,
+                                  double* scores, hipStream_t stream);
 
 /*
  * Scratch bytes spade_block_sparse_attn needs for its work schedule (the

@@ -256,9 +256,122 @@ spade_status spade_estimate_select(const spade_geom* g, const double* qbar, cons
     return fail(SPADE_ERR_INVALID_ARG, "qbar, kbar, counts and indices must be non-null");
   if (!aligned16(qbar) || !aligned16(kbar))
     return fail(SPADE_ERR_INVALID_ARG, "qbar and kbar must be 16-byte aligned");
-  return hip_status(spade::launch_estimate_select(dg, qbar, kbar, mode, topk, tau, scale, counts,
-                                                  indices, scores, stream),
-                    "estimate_select launch");
+  spade::SelectSpec p = {};
+  p.q0 = qbar;
+  p.k0 = kbar;
+  p.estimator = spade::kEstMean;
+  p.mode = mode;
+  p.topk = topk;
+  p.tau = tau;
+  p.scale = scale;
+  p.intra = spade::kIntraNone;
+  p.wt = p.wh = p.ww = -1;
+  p.counts = counts;
+  p.indices = indices;
+  p.scores = scores;
+  return hip_status(spade::launch_select(dg, p, stream), "estimate_select launch");
+}
+
+spade_status spade_block_minmax(const spade_geom* g, const void* q, const void* k, double* qmax,
+                                double* qmin, double* kmax, double* kmin, double* sics_q,
+                                double* sics_k, const int32_t* heads, int32_t n_heads,
+                                hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if ((sics_q == nullptr) != (sics_k == nullptr))
+    return fail(SPADE_ERR_INVALID_ARG, "sics_q and sics_k must both be given or both be null");
+  spade::HeadMap hm;
+  st = parse_heads(dg, heads, n_heads, &hm);
+  if (st != SPADE_OK) return st;
+  if (empty || hm.n == 0) return SPADE_OK;
+  if (!q || !k || !qmax || !qmin || !kmax || !kmin)
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, qmax, qmin, kmax and kmin must be non-null");
+  if (!aligned16(q) || !aligned16(k))
+    return fail(SPADE_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  return hip_status(spade::launch_block_minmax(dg, hm, q, k, qmax, qmin, kmax, kmin, sics_q,
+                                               sics_k, stream),
+                    "block_minmax launch");
+}
+
+spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* spec,
+                                  const spade_summaries* sum, int32_t* counts, int32_t* indices,
+                                  double* scores, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (!spec || !sum) return fail(SPADE_ERR_INVALID_ARG, "spec and summaries must be non-null");
+  const spade_mask_spec& m = *spec;
+  if (m.estimator != SPADE_EST_MEAN && m.estimator != SPADE_EST_DSA &&
+      m.estimator != SPADE_EST_DSA2)
+    return fail(SPADE_ERR_INVALID_ARG, "estimator must be SPADE_EST_MEAN, _DSA or _DSA2 (got %d)",
+                m.estimator);
+  if (m.mode != SPADE_TOPK && m.mode != SPADE_TOPP)
+    return fail(SPADE_ERR_INVALID_ARG, "mode must be SPADE_TOPK or SPADE_TOPP (got %d)", m.mode);
+  if (m.mode == SPADE_TOPK && !m.topk_per_head && m.topk < 1)
+    return fail(SPADE_ERR_INVALID_ARG, "topk must be >= 1 (got %d)", m.topk);
+  if (m.mode == SPADE_TOPP && !m.tau_per_head && !(m.tau > 0.0 && m.tau <= 1.0))
+    return fail(SPADE_ERR_INVALID_ARG, "tau must lie in (0, 1] (got %g)", m.tau);
+  if (!(isfinite(m.scale) && m.scale > 0.0))
+    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", m.scale);
+  if (m.intra != SPADE_INTRA_NONE && m.intra != SPADE_INTRA_THRESHOLD &&
+      m.intra != SPADE_INTRA_TOPK)
+    return fail(SPADE_ERR_INVALID_ARG, "intra must be SPADE_INTRA_NONE, _THRESHOLD or _TOPK (got %d)",
+                m.intra);
+  if (m.intra == SPADE_INTRA_TOPK && m.intra_topk < 0)
+    return fail(SPADE_ERR_INVALID_ARG, "intra_topk must be >= 0 (got %d)", m.intra_topk);
+  if (m.intra == SPADE_INTRA_THRESHOLD && isnan(m.intra_theta))
+    return fail(SPADE_ERR_INVALID_ARG, "intra_theta must not be NaN");
+  if (m.sink_tokens < 0)
+    return fail(SPADE_ERR_INVALID_ARG, "sink_tokens must be >= 0 (got %lld)",
+                (long long)m.sink_tokens);
+  if (!empty && dg.NB > spade::kMaxSelectNB)
+    return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the selection limit %d", dg.NB,
+                spade::kMaxSelectNB);
+  if (empty) return SPADE_OK;
+  if (!counts || !indices)
+    return fail(SPADE_ERR_INVALID_ARG, "counts and indices must be non-null");
+  spade::SelectSpec p = {};
+  if (m.estimator == SPADE_EST_MEAN) {
+    if (!sum->qbar || !sum->kbar)
+      return fail(SPADE_ERR_INVALID_ARG, "the mean estimator needs qbar and kbar");
+    p.q0 = sum->qbar;
+    p.k0 = sum->kbar;
+  } else {
+    if (!sum->qmax || !sum->qmin || !sum->kmax || !sum->kmin)
+      return fail(SPADE_ERR_INVALID_ARG, "the DSA estimators need qmax, qmin, kmax and kmin");
+    p.q0 = sum->qmax;
+    p.q1 = sum->qmin;
+    p.k0 = sum->kmax;
+    p.k1 = sum->kmin;
+  }
+  if (!aligned16(p.q0) || !aligned16(p.k0) || (p.q1 && (!aligned16(p.q1) || !aligned16(p.k1))))
+    return fail(SPADE_ERR_INVALID_ARG, "summaries must be 16-byte aligned");
+  if (m.intra != SPADE_INTRA_NONE && (!sum->sics_q || !sum->sics_k))
+    return fail(SPADE_ERR_INVALID_ARG, "the intra-block filter needs sics_q and sics_k");
+  p.sics_q = sum->sics_q;
+  p.sics_k = sum->sics_k;
+  p.topk_h = m.topk_per_head;
+  p.tau_h = m.tau_per_head;
+  p.estimator = m.estimator;
+  p.mode = m.mode;
+  p.topk = m.topk;
+  p.tau = m.tau;
+  p.scale = m.scale;
+  p.intra = m.intra;
+  p.intra_k = m.intra_topk;
+  p.intra_theta = m.intra_theta;
+  const bool window = m.window[0] >= 0 && m.window[1] >= 0 && m.window[2] >= 0;
+  p.wt = window ? m.window[0] : -1;
+  p.wh = window ? m.window[1] : -1;
+  p.ww = window ? m.window[2] : -1;
+  p.sink = m.sink_tokens;
+  p.counts = counts;
+  p.indices = indices;
+  p.scores = scores;
+  return hip_status(spade::launch_select(dg, p, stream), "compose_select launch");
 }
 
 size_t spade_attn_workspace_bytes(const spade_geom* g) {

@@ -1,10 +1,19 @@
 // Inter-block Estimator + Top-K / Top-P index search (paper §3.3; Top-K/Top-P
-// mode of §3.1) on gfx950.
+// mode of §3.1), composed with the intra-block filter, the local window and the
+// attention sink (§3.1 sparsity-ratio scheme and utility parameters; §3.3: intra
+// scores broadcast and OR-combined with the inter ones, the result united with
+// the window and sink masks), on gfx950.
 //
 // One workgroup (8 waves) owns 16 query-block rows of one head.
-//  1. Scores: the 16 x NB tile S = qbar kbar^T * scale is computed in fp64 with
-//     v_mfma_f64_16x16x4 and parked in LDS. The contraction index is permuted so
-//     each lane streams 16-byte pieces of the summary rows.
+//  1. Scores, the 16 x NB tile parked in LDS, in fp64:
+//     MEAN  S = qbar kbar^T * scale with v_mfma_f64_16x16x4. The contraction
+//           index is permuted so each lane streams 16-byte pieces of the rows.
+//     DSA   per channel max(q~ k_max, q~ k_min) with q~ the query block's
+//           midpoint, summed: equal to <q~, k_c> + <|q~|, k_r> (k_c, k_r the key
+//           box's centre and half width), so the same MFMA contraction runs
+//           over 2d terms.
+//     DSA2  per channel the largest product of a query and a key extreme: not
+//           a contraction (the max is inside the sum), so plain fp64 VALU.
 //  2. Selection: one wave per row. Each row's scores are mapped to order-
 //     preserving 64-bit keys held in registers (element e = 64*s + lane). The
 //     cut key t* = max{t : W(key >= t) >= need} is found by a most-significant-
@@ -14,7 +23,13 @@
 //     softmax numerators exp(s - max) in 2^-53 fixed point, so bucket sums are
 //     exact integers independent of summation order (need = ceil(tau * Z)).
 //     Blocks with key > t* are kept; blocks tied at t* are taken in ascending
-//     index order until the rule is met. Kept indices are written ascending.
+//     index order until the rule is met.
+//  3. Composition: a block is kept when the inter rule keeps it, when its query
+//     block or its key block is marked by the intra filter (incoherent: SICS/n^2
+//     below a threshold, or among the k least coherent of the head, found with
+//     the same radix cut), when it lies in the query block's window, or when it
+//     holds one of the first `sink` raster tokens. Kept indices are written
+//     ascending.
 #include "spade_internal.h"
 
 namespace spade {
@@ -72,77 +87,318 @@ __device__ __forceinline__ int lanes_below(uint64_t ballot) {
                                    __builtin_amdgcn_mbcnt_lo(uint32_t(ballot), 0));
 }
 
-template <int D>
-__global__ void __launch_bounds__(kThreads)
-    estimate_select_kernel(DevGeom g, const double* __restrict__ qbar,
-                           const double* __restrict__ kbar, int mode, int topk, double tau,
-                           double scale, int* __restrict__ counts, int* __restrict__ indices,
-                           double* __restrict__ scores_out) {
+// Result of one wave's cut: keep keys > tstar, and the first `take` keys equal
+// to tstar in ascending element order; all = keep every element.
+struct Cut {
+  uint64_t tstar;
+  long long take;
+  bool all;
+};
+
+// Radix search of one wave's keys (0 = no element) with weights w for the
+// largest t with W(key >= t) >= need. count_rule: the tie group fills the count
+// (Top-K); otherwise the mass (Top-P). hw/hc: this wave's LDS histograms.
+__device__ Cut find_cut(const uint64_t (&key)[kMaxS], const uint64_t (&w)[kMaxS], uint64_t need,
+                        bool count_rule, uint64_t* hw, unsigned* hc, int lane) {
+  uint64_t prefix = 0, above = 0, tstar = 0;
+  for (int pass = 0; pass < 8; ++pass) {
+    const int shift = 56 - 8 * pass;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      hw[4 * lane + q] = 0;
+      hc[4 * lane + q] = 0;
+    }
+    wave_sync();
+#pragma unroll
+    for (int s = 0; s < kMaxS; ++s) {
+      const bool cand =
+          key[s] != 0 && (pass == 0 || (key[s] >> (shift + 8)) == (prefix >> (shift + 8)));
+      if (cand) {
+        const int dg = int((key[s] >> shift) & 255u);
+        atomicAdd(reinterpret_cast<unsigned long long*>(&hw[dg]), (unsigned long long)w[s]);
+        atomicAdd(&hc[dg], 1u);
+      }
+    }
+    wave_sync();
+    uint64_t bw[4], loc[4];
+    unsigned bc[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      bw[q] = hw[4 * lane + q];
+      bc[q] = hc[4 * lane + q];
+    }
+    loc[3] = bw[3];
+    loc[2] = loc[3] + bw[2];
+    loc[1] = loc[2] + bw[1];
+    loc[0] = loc[1] + bw[0];
+    const uint64_t E = wave_suffix_excl_u64(loc[0], lane);
+    int bq = -1;
+#pragma unroll
+    for (int q = 3; q >= 0; --q)
+      if (bq < 0 && above + E + loc[q] >= need) bq = q;
+    const uint64_t has = __ballot(bq >= 0);
+    if (has == 0) return {0, 0, true};  // total weight below need
+    const int L = 63 - __builtin_clzll(has);
+    uint64_t my_suf = 0, my_w = 0;
+    unsigned my_c = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      if (q == bq) {
+        my_suf = E + loc[q];
+        my_w = bw[q];
+        my_c = bc[q];
+      }
+    const int q_L = __shfl(bq, L, 64);
+    const uint64_t suf = __shfl(my_suf, L, 64);
+    const uint64_t wD = __shfl(my_w, L, 64);
+    const unsigned cD = __shfl(my_c, L, 64);
+    const int Dg = 4 * L + q_L;
+    prefix |= uint64_t(Dg) << shift;
+    if (cD == 1) {  // a single element in the bucket: its key is the cut
+      uint64_t kk = 0;
+#pragma unroll
+      for (int s = 0; s < kMaxS; ++s)
+        if (key[s] != 0 && (key[s] >> shift) == (prefix >> shift)) kk = key[s];
+      tstar = wave_max_u64(kk);
+      break;
+    }
+    if (pass == 7) {  // all 64 bits fixed: a group of equal keys
+      tstar = prefix;
+      break;
+    }
+    above += suf - wD;
+  }
+  // elements strictly above the cut, and the tie group at the cut
+  int n_above = 0, n_tie = 0;
+  uint64_t w_above = 0, w_tie = 0;
+#pragma unroll
+  for (int s = 0; s < kMaxS; ++s) {
+    const bool gt = key[s] > tstar, eq = key[s] == tstar;
+    n_above += __popcll(__ballot(gt));
+    n_tie += __popcll(__ballot(eq));
+    if (gt) w_above += w[s];
+    if (eq) w_tie = w[s];
+  }
+  w_above = wave_sum_u64(w_above);
+  w_tie = wave_max_u64(w_tie);
+  long long take;
+  if (count_rule) {
+    take = (long long)need - n_above;
+  } else {
+    const uint64_t rem = need > w_above ? need - w_above : 0;
+    take = w_tie > 0 ? (long long)((rem + w_tie - 1) / w_tie) : n_tie;
+  }
+  take = take < 1 ? 1 : (take > n_tie ? n_tie : take);
+  return {tstar, take, false};
+}
+
+// Block-grid coordinates packed as (tb << 20) | (hb << 10) | wb (each < 1024
+// because NB <= 1024).
+__device__ __forceinline__ int pack_coords(const DevGeom& g, int b) {
+  const int wb = b % g.nW, r = b / g.nW;
+  return ((r / g.nH) << 20) | ((r % g.nH) << 10) | wb;
+}
+
+__device__ __forceinline__ bool in_window(int ci, int cj, int wt, int wh, int ww) {
+  return abs((ci >> 20) - (cj >> 20)) <= wt && abs(((ci >> 10) & 1023) - ((cj >> 10) & 1023)) <= wh &&
+         abs((ci & 1023) - (cj & 1023)) <= ww;
+}
+
+// coherence SICS / n^2 of block b (intra-block filter input)
+__device__ __forceinline__ double coherence(const DevGeom& g, const double* sics, int b) {
+  const double n = double(block_ext(g, b).n);
+  return sics[b] / (n * n);
+}
+
+// Marks of the intra Top-K filter over one head's blocks: the `k` least
+// coherent (ties to the lower index), written as 1s into mark[e - lo] for
+// lo <= e < hi. One wave.
+__device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, int lo, int hi,
+                                 unsigned char* mark, uint64_t* hw, unsigned* hc, int lane) {
+  const int NB = g.NB;
+  uint64_t key[kMaxS], w[kMaxS];
+#pragma unroll
+  for (int s = 0; s < kMaxS; ++s) {
+    const int e = s * 64 + lane;
+    key[s] = e < NB ? order_key(-coherence(g, sics, e) + 0.0) : 0;  // least coherent first
+    w[s] = key[s] != 0 ? 1 : 0;
+  }
+  const Cut c = find_cut(key, w, uint64_t(min(k, NB)), true, hw, hc, lane);
+  int tie_base = 0;
+#pragma unroll
+  for (int s = 0; s < kMaxS; ++s) {
+    const int e = s * 64 + lane;
+    const bool eq = key[s] != 0 && key[s] == c.tstar;
+    const uint64_t be = __ballot(eq);
+    const int tr = tie_base + lanes_below(be);
+    tie_base += __popcll(be);
+    const bool kept = key[s] != 0 && (c.all || key[s] > c.tstar || (eq && tr < c.take));
+    if (kept && e >= lo && e < hi) mark[e - lo] = 1;
+  }
+}
+
+template <int D, int EST>
+__global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec p) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int NB = g.NB;
   double* sc = reinterpret_cast<double*>(smem);                           // [kRows][NB]
   uint64_t* hist_w = reinterpret_cast<uint64_t*>(sc + kRows * NB);         // [kWaves][256]
   unsigned* hist_c = reinterpret_cast<unsigned*>(hist_w + kWaves * 256);  // [kWaves][256]
+  int* coord = reinterpret_cast<int*>(hist_c + kWaves * 256);             // [NB]
+  unsigned char* colmark = reinterpret_cast<unsigned char*>(coord + NB);  // [NB]
+  unsigned char* rowmark = colmark + NB;                                  // [kRows]
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i0 = blockIdx.x * kRows;
   const int64_t bh = blockIdx.y;
-  const double* qh = qbar + bh * NB * D;
-  const double* kh = kbar + bh * NB * D;
+  const int h = int(bh % g.H);
+  const double* q0 = p.q0 + bh * NB * D;
+  const double* k0 = p.k0 + bh * NB * D;
 
-  // ---------------- phase 1: scores (fp64 MFMA) ----------------
-  // MFMA step (kq, h) contracts d = 8*kq + 2*g4 + h, g4 = lane/16 the k-slot.
+  // ---------------- phase 1: scores ----------------
   constexpr int KQ = D / 8;
   const int r16 = lane & 15, g4 = lane >> 4;
-  double qa[2 * KQ];
-  {
-    const int row = i0 + r16;
-    const double2* p = reinterpret_cast<const double2*>(qh + int64_t(min(row, NB - 1)) * D) + g4;
-#pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) {
-      const double2 v = p[4 * kq];
-      qa[2 * kq] = row < NB ? v.x : 0.0;
-      qa[2 * kq + 1] = row < NB ? v.y : 0.0;
-    }
-  }
   const int ntiles = (NB + 15) / 16;
-  for (int jt = wave; jt < ntiles; jt += kWaves) {
-    const int col = jt * 16 + r16;
-    const double2* p = reinterpret_cast<const double2*>(kh + int64_t(min(col, NB - 1)) * D) + g4;
-    double2 kv[KQ];
+  if (EST != kEstDsa2) {
+    // MFMA step (kq, h) contracts d = 8*kq + 2*g4 + h, g4 = lane/16 the k-slot.
+    // DSA: A = q~ = (qmax + qmin)/2 against B = k_c, then |q~| against k_r.
+    double qa[2 * KQ];
+    {
+      const int row = i0 + r16;
+      const int64_t ro = int64_t(min(row, NB - 1)) * D;
+      const double2* p0 = reinterpret_cast<const double2*>(q0 + ro) + g4;
+      const double2* p1 = EST == kEstDsa ? reinterpret_cast<const double2*>(p.q1 + bh * NB * D + ro) + g4
+                                         : nullptr;
 #pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) kv[kq] = p[4 * kq];
-    f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll
-    for (int kq = 0; kq < KQ; ++kq) {
-      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq], kv[kq].x, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq + 1], kv[kq].y, acc, 0, 0, 0);
+      for (int kq = 0; kq < KQ; ++kq) {
+        double2 v = p0[4 * kq];
+        if (EST == kEstDsa) {
+          const double2 u = p1[4 * kq];
+          v.x = (v.x + u.x) * 0.5;
+          v.y = (v.y + u.y) * 0.5;
+        }
+        qa[2 * kq] = row < NB ? v.x : 0.0;
+        qa[2 * kq + 1] = row < NB ? v.y : 0.0;
+      }
     }
-    if (col < NB) {
+    for (int jt = wave; jt < ntiles; jt += kWaves) {
+      const int col = jt * 16 + r16;
+      const int64_t co = int64_t(min(col, NB - 1)) * D;
+      const double2* pk = reinterpret_cast<const double2*>(k0 + co) + g4;
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      if (EST == kEstMean) {
+        double2 kv[KQ];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {  // acc[r] = S[4r + g4][r16]
-        const int rr = 4 * r + g4;
-        const double s = acc[r] * scale + 0.0;  // + 0.0 folds -0 into +0
-        sc[rr * NB + col] = s;
-        if (scores_out && i0 + rr < NB) scores_out[(bh * NB + i0 + rr) * NB + col] = s;
+        for (int kq = 0; kq < KQ; ++kq) kv[kq] = pk[4 * kq];
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) {
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq], kv[kq].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq + 1], kv[kq].y, acc, 0, 0, 0);
+        }
+      } else {
+        const double2* pn = reinterpret_cast<const double2*>(p.k1 + bh * NB * D + co) + g4;
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) {
+          const double2 a = pk[4 * kq], b = pn[4 * kq];
+          const double cx = (a.x + b.x) * 0.5, cy = (a.y + b.y) * 0.5;  // centre (exact)
+          const double rx = (a.x - b.x) * 0.5, ry = (a.y - b.y) * 0.5;  // half width (exact)
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq], cx, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq + 1], cy, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(fabs(qa[2 * kq]), rx, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(fabs(qa[2 * kq + 1]), ry, acc, 0, 0, 0);
+        }
+      }
+      if (col < NB) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {  // acc[r] = S[4r + g4][r16]
+          const int rr = 4 * r + g4;
+          const double s = acc[r] * p.scale + 0.0;  // + 0.0 folds -0 into +0
+          sc[rr * NB + col] = s;
+          if (p.scores && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
+        }
+      }
+    }
+  } else {
+    // DSA2 on the VALU: lane (r16, g4) scores column jt*16 + r16 against rows
+    // 4r + g4, summing channels in order.
+    const double* q1 = p.q1 + bh * NB * D;
+    const double* k1 = p.k1 + bh * NB * D;
+    for (int jt = wave; jt < ntiles; jt += kWaves) {
+      const int col = jt * 16 + r16;
+      const int64_t co = int64_t(min(col, NB - 1)) * D;
+      double acc[4] = {0.0, 0.0, 0.0, 0.0};
+      int64_t ro[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) ro[r] = int64_t(min(i0 + 4 * r + g4, NB - 1)) * D;
+      for (int c = 0; c < D; c += 2) {
+        const double2 kx = *reinterpret_cast<const double2*>(k0 + co + c);
+        const double2 kn = *reinterpret_cast<const double2*>(k1 + co + c);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const double2 qx = *reinterpret_cast<const double2*>(q0 + ro[r] + c);
+          const double2 qn = *reinterpret_cast<const double2*>(q1 + ro[r] + c);
+          acc[r] += fmax(fmax(qx.x * kx.x, qx.x * kn.x), fmax(qn.x * kx.x, qn.x * kn.x));
+          acc[r] += fmax(fmax(qx.y * kx.y, qx.y * kn.y), fmax(qn.y * kx.y, qn.y * kn.y));
+        }
+      }
+      if (col < NB) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int rr = 4 * r + g4;
+          const double s = acc[r] * p.scale + 0.0;
+          sc[rr * NB + col] = s;
+          if (p.scores && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
+        }
       }
     }
   }
+
+  // ---------------- composition inputs ----------------
+  const bool window = p.wt >= 0;
+  const bool extras = p.intra != kIntraNone || window || p.sink > 0;
+  if (extras) {
+    const double* sk = p.sics_k ? p.sics_k + bh * NB : nullptr;
+    for (int j = threadIdx.x; j < NB; j += kThreads) {
+      bool m = false;
+      if (p.sink > 0) {
+        const BlockExt e = block_ext(g, j);
+        m = (int64_t(e.t0) * g.Hs + e.y0) * g.Ws + e.x0 < p.sink;  // its first raster token
+      }
+      if (p.intra == kIntraThreshold) m = m || coherence(g, sk, j) < p.intra_theta;
+      colmark[j] = m;
+      if (window) coord[j] = pack_coords(g, j);
+    }
+    if (threadIdx.x < kRows) {
+      const int row = i0 + threadIdx.x;
+      rowmark[threadIdx.x] = p.intra == kIntraThreshold && row < NB &&
+                             coherence(g, p.sics_q + bh * NB, row) < p.intra_theta;
+    }
+  }
   __syncthreads();
+  if (p.intra == kIntraTopk && p.intra_k > 0) {
+    if (wave == 0)
+      intra_topk_marks(g, p.sics_k + bh * NB, p.intra_k, 0, NB, colmark, hist_w, hist_c, lane);
+    else if (wave == 1)
+      intra_topk_marks(g, p.sics_q + bh * NB, p.intra_k, i0, i0 + kRows, rowmark, hist_w + 256,
+                       hist_c + 256, lane);
+    __syncthreads();
+  }
 
   // ---------------- phase 2: one wave per row ----------------
   const int S = (NB + 63) / 64;
   uint64_t* hw = hist_w + wave * 256;
   unsigned* hc = hist_c + wave * 256;
+  const int topk = p.topk_h ? min(max(p.topk_h[h], 1), NB) : p.topk;
+  const double tau = p.tau_h ? p.tau_h[h] : p.tau;
   for (int rr = wave; rr < kRows; rr += kWaves) {
     const int row = i0 + rr;
     if (row >= NB) break;  // uniform per wave; no block barrier below
     const int64_t rowid = bh * NB + row;
-    int* out = indices + rowid * NB;
+    int* out = p.indices + rowid * NB;
 
-    if (mode == 1 && tau >= 1.0) {  // Top-P with tau = 1 keeps every block
+    if ((p.mode == 1 && tau >= 1.0) || (extras && rowmark[rr])) {  // every block kept
       for (int e = lane; e < NB; e += 64) out[e] = e;
-      if (lane == 0) counts[rowid] = NB;
+      if (lane == 0) p.counts[rowid] = NB;
       continue;
     }
 
@@ -160,7 +416,7 @@ __global__ void __launch_bounds__(kThreads)
       }
     }
     uint64_t need;
-    if (mode == 0) {
+    if (p.mode == 0) {
 #pragma unroll
       for (int s = 0; s < kMaxS; ++s) w[s] = key[s] != 0 ? 1 : 0;
       need = uint64_t(min(topk, NB));
@@ -177,153 +433,71 @@ __global__ void __launch_bounds__(kThreads)
         }
       }
       z = wave_sum_u64(z);
-      need = uint64_t(ceil(tau * double(z)));
+      const double t = tau > 0.0 ? tau : 0.0;  // NaN or <= 0: the top block only
+      need = uint64_t(ceil(t * double(z)));
       need = need < 1 ? 1 : (need > z ? z : need);
     }
-
-    // MSD radix search for t* = max{t : sum_{key >= t} w >= need}
-    uint64_t prefix = 0, above = 0, tstar = 0;
-    bool keep_all = false;
-    for (int pass = 0; pass < 8; ++pass) {
-      const int shift = 56 - 8 * pass;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        hw[4 * lane + q] = 0;
-        hc[4 * lane + q] = 0;
-      }
-      wave_sync();
-#pragma unroll
-      for (int s = 0; s < kMaxS; ++s) {
-        const bool cand = key[s] != 0 && (pass == 0 || (key[s] >> (shift + 8)) == (prefix >> (shift + 8)));
-        if (cand) {
-          const int dg = int((key[s] >> shift) & 255u);
-          atomicAdd(reinterpret_cast<unsigned long long*>(&hw[dg]), (unsigned long long)w[s]);
-          atomicAdd(&hc[dg], 1u);
-        }
-      }
-      wave_sync();
-      uint64_t bw[4], loc[4];
-      unsigned bc[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        bw[q] = hw[4 * lane + q];
-        bc[q] = hc[4 * lane + q];
-      }
-      loc[3] = bw[3];
-      loc[2] = loc[3] + bw[2];
-      loc[1] = loc[2] + bw[1];
-      loc[0] = loc[1] + bw[0];
-      const uint64_t E = wave_suffix_excl_u64(loc[0], lane);
-      int bq = -1;
-#pragma unroll
-      for (int q = 3; q >= 0; --q)
-        if (bq < 0 && above + E + loc[q] >= need) bq = q;
-      const uint64_t has = __ballot(bq >= 0);
-      if (has == 0) {  // total weight below need (cannot happen for valid rules)
-        keep_all = true;
-        break;
-      }
-      const int L = 63 - __builtin_clzll(has);
-      // values of the chosen lane
-      uint64_t my_suf = 0, my_w = 0;
-      unsigned my_c = 0;
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (q == bq) {
-          my_suf = E + loc[q];
-          my_w = bw[q];
-          my_c = bc[q];
-        }
-      const int q_L = __shfl(bq, L, 64);
-      const uint64_t suf = __shfl(my_suf, L, 64);
-      const uint64_t wD = __shfl(my_w, L, 64);
-      const unsigned cD = __shfl(my_c, L, 64);
-      const int Dg = 4 * L + q_L;
-      prefix |= uint64_t(Dg) << shift;
-      if (cD == 1) {  // a single element in the bucket: its key is the cut
-        uint64_t kk = 0;
-#pragma unroll
-        for (int s = 0; s < kMaxS; ++s)
-          if (key[s] != 0 && (key[s] >> shift) == (prefix >> shift)) kk = key[s];
-        tstar = wave_max_u64(kk);
-        break;
-      }
-      if (pass == 7) {  // all 64 bits fixed: a group of equal keys
-        tstar = prefix;
-        break;
-      }
-      above += suf - wD;
-    }
+    const Cut c = find_cut(key, w, need, p.mode == 0, hw, hc, lane);
 
     int cnt_out = 0;
-    if (keep_all) {
+    if (c.all) {
       for (int e = lane; e < NB; e += 64) out[e] = e;
       cnt_out = NB;
     } else {
-      // elements strictly above the cut, and the tie group at the cut
-      int n_above = 0, n_tie = 0;
-      uint64_t w_above = 0, w_tie = 0;
-#pragma unroll
-      for (int s = 0; s < kMaxS; ++s) {
-        const bool gt = key[s] > tstar, eq = key[s] == tstar;
-        n_above += __popcll(__ballot(gt));
-        n_tie += __popcll(__ballot(eq));
-        if (gt) w_above += w[s];
-        if (eq) w_tie = w[s];
-      }
-      w_above = wave_sum_u64(w_above);
-      w_tie = wave_max_u64(w_tie);
-      long long take;
-      if (mode == 0) {
-        take = (long long)need - n_above;
-      } else {
-        const uint64_t rem = need > w_above ? need - w_above : 0;
-        take = w_tie > 0 ? (long long)((rem + w_tie - 1) / w_tie) : n_tie;
-      }
-      take = take < 1 ? 1 : (take > n_tie ? n_tie : take);
+      const int ci = window ? coord[row] : 0;
       int tie_base = 0;
 #pragma unroll
       for (int s = 0; s < kMaxS; ++s) {
-        const bool eq = key[s] == tstar;
+        const int e = s * 64 + lane;
+        const bool eq = key[s] == c.tstar;
         const uint64_t be = __ballot(eq);
         const int tr = tie_base + lanes_below(be);
         tie_base += __popcll(be);
-        const bool kept = key[s] > tstar || (eq && tr < take);
+        bool kept = key[s] > c.tstar || (eq && tr < c.take);
+        if (extras && !kept && s < S && e < NB)
+          kept = colmark[e] || (window && in_window(ci, coord[e], p.wt, p.wh, p.ww));
         const uint64_t bk = __ballot(kept);
-        if (kept) out[cnt_out + lanes_below(bk)] = s * 64 + lane;
+        if (kept) out[cnt_out + lanes_below(bk)] = e;
         cnt_out += __popcll(bk);
       }
     }
-    if (lane == 0) counts[rowid] = cnt_out;
+    if (lane == 0) p.counts[rowid] = cnt_out;
   }
 }
 
-template <int D>
-hipError_t launch_d(const DevGeom& g, const double* qbar, const double* kbar, int mode, int topk,
-                    double tau, double scale, int* counts, int* indices, double* scores,
-                    hipStream_t s) {
-  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * (8 + 4);
+template <int D, int EST>
+hipError_t launch_de(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
+  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * (8 + 4) +
+                     size_t(g.NB) * (4 + 1) + kRows;
   static bool attr_set = false;  // raising the dynamic-LDS cap once is idempotent
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&estimate_select_kernel<D>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 12));
+    hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&select_kernel<D, EST>),
+        hipFuncAttributeMaxDynamicSharedMemorySize,
+        int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 12 + kMaxSelectNB * 5 + kRows));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const dim3 grid((g.NB + kRows - 1) / kRows, g.B * g.H);
-  estimate_select_kernel<D><<<grid, kThreads, lds, s>>>(g, qbar, kbar, mode, topk, tau, scale,
-                                                        counts, indices, scores);
+  select_kernel<D, EST><<<grid, kThreads, lds, s>>>(g, p);
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
+  switch (p.estimator) {
+    case kEstMean: return launch_de<D, kEstMean>(g, p, s);
+    case kEstDsa: return launch_de<D, kEstDsa>(g, p, s);
+    case kEstDsa2: return launch_de<D, kEstDsa2>(g, p, s);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const double* kbar,
-                                  int mode, int topk, double tau, double scale, int* counts,
-                                  int* indices, double* scores, hipStream_t s) {
-  if (g.d == 128) return launch_d<128>(g, qbar, kbar, mode, topk, tau, scale, counts, indices, scores, s);
-  if (g.d == 64) return launch_d<64>(g, qbar, kbar, mode, topk, tau, scale, counts, indices, scores, s);
+hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
+  if (g.d == 128) return launch_d<128>(g, p, s);
+  if (g.d == 64) return launch_d<64>(g, p, s);
   return hipErrorInvalidValue;
 }
 

@@ -82,11 +82,35 @@ hipError_t launch_choose_scheme(const double* as_qk, int C, int B, int H, int* c
 hipError_t launch_block_summarize(const DevGeom& g, const HeadMap& hm, const void* q,
                                   const void* k, void* qb, void* kb, double* qbar, double* kbar,
                                   double* sics_q, double* sics_k, hipStream_t s);
+hipError_t launch_block_minmax(const DevGeom& g, const HeadMap& hm, const void* q, const void* k,
+                               double* qmax, double* qmin, double* kmax, double* kmin,
+                               double* sics_q, double* sics_k, hipStream_t s);
 hipError_t launch_summarize(const DevGeom& g, const void* qb, const void* kb, double* qbar,
                             double* kbar, double* sics_q, double* sics_k, hipStream_t s);
-hipError_t launch_estimate_select(const DevGeom& g, const double* qbar, const double* kbar,
-                                  int mode, int topk, double tau, double scale, int* counts,
-                                  int* indices, double* scores, hipStream_t s);
+// One selection call (estimator, row rule, intra filter, window, sink), as the
+// kernel sees it; validated and normalised by the C-ABI layer.
+enum { kEstMean = 0, kEstDsa = 1, kEstDsa2 = 2 };
+enum { kIntraNone = 0, kIntraThreshold = 1, kIntraTopk = 2 };
+struct SelectSpec {
+  const double* q0;  // MEAN: qbar; DSA, DSA2: qmax
+  const double* q1;  // DSA, DSA2: qmin
+  const double* k0;  // MEAN: kbar; DSA, DSA2: kmax
+  const double* k1;  // DSA, DSA2: kmin
+  const double* sics_q;
+  const double* sics_k;
+  const int* topk_h;     // per-head k (nullable)
+  const double* tau_h;   // per-head tau (nullable)
+  int estimator, mode, topk;
+  double tau, scale;
+  int intra, intra_k;
+  double intra_theta;
+  int wt, wh, ww;        // window radii in blocks; wt < 0: no window
+  int64_t sink;          // attention-sink length in tokens (0: none)
+  int* counts;
+  int* indices;
+  double* scores;
+};
+hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
 size_t attn_workspace_bytes(const DevGeom& g);
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,

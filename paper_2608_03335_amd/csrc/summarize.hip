@@ -1,5 +1,6 @@
-// Summarizer (block mean, paper §3.1 MEAN-SPADE) and intra-block estimator SICS
-// (§3.2, Eq. (4)-(5), Alg. 1) over the blocked bf16 layout.
+// Summarizer (block mean, paper §3.1 MEAN-SPADE; block max/min for the DSA
+// estimators) and intra-block estimator SICS (§3.2, Eq. (4)-(5), Alg. 1) over
+// the blocked bf16 layout or straight from the raster layout.
 //
 // One workgroup per (block, head) reads that block's Q rows, then its K rows.
 // Lane layout: V = d/8 lanes share one token row (16 bytes = 8 bf16 each), so
@@ -198,6 +199,116 @@ __global__ void __launch_bounds__(kThreads) block_summarize_kernel(
   }
 }
 
+// Max/min Summarizer (§3.1: the summaries DSA-SPADE's estimators take) and SICS
+// in one pass over the raster tensors: per block, the elementwise max and min
+// of its real rows of Q, then K. bf16 values are exact in fp32, so the extremes
+// are exact; SICS is accumulated exactly as block_summarize_kernel does (same
+// rows, same operations, same order), so the two calls agree bit for bit.
+template <int D, bool SICS>
+__global__ void __launch_bounds__(kThreads) block_minmax_kernel(
+    DevGeom g, HeadMap hm, const uint4* __restrict__ q, const uint4* __restrict__ k,
+    double* __restrict__ qmax, double* __restrict__ qmin, double* __restrict__ kmax,
+    double* __restrict__ kmin, double* __restrict__ sics_q, double* __restrict__ sics_k) {
+  constexpr int V = D / 8;
+  constexpr int G = kThreads / V;
+  __shared__ float pmax[G][D];
+  __shared__ float pmin[G][D];
+  __shared__ double upart[SICS ? G : 1][SICS ? D : 1];
+  __shared__ double sq[kThreads / 64];
+
+  const int b = blockIdx.x;
+  int64_t bh_blk, bh_ras;
+  head_pair(g, hm, &bh_blk, &bh_ras);
+  const BlockExt e = block_ext(g, b);
+  const int n = e.n;
+  const float r_ew = 1.0f / float(e.ew), r_eh = 1.0f / float(e.eh);
+  const int vec = threadIdx.x % V, grp = threadIdx.x / V;
+
+  for (int which = 0; which < 2; ++which) {
+    const uint4* src = (which ? k : q) + bh_ras * g.N * V;
+    float mx[8], mn[8];
+    double uacc[8];
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      mx[c] = -INFINITY;
+      mn[c] = INFINITY;
+      uacc[c] = 0.0;
+    }
+#pragma unroll 2
+    for (int s = grp; s < n; s += G) {
+      float f[8];
+      bf16x8_to_f32(src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec], f);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        mx[c] = fmaxf(mx[c], f[c]);
+        mn[c] = fminf(mn[c], f[c]);
+      }
+      if (SICS) {
+        double ss = 0.0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) ss += double(f[c]) * double(f[c]);
+#pragma unroll
+        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
+        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) uacc[c] += double(f[c]) * inv;
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      pmax[grp][vec * 8 + c] = mx[c];
+      pmin[grp][vec * 8 + c] = mn[c];
+      if (SICS) upart[grp][vec * 8 + c] = uacc[c];
+    }
+    __syncthreads();
+    double u2 = 0.0;
+    if (threadIdx.x < D) {
+      const int c = threadIdx.x;
+      float a = pmax[0][c], z = pmin[0][c];
+      for (int r = 1; r < G; ++r) {
+        a = fmaxf(a, pmax[r][c]);
+        z = fminf(z, pmin[r][c]);
+      }
+      const int64_t o = (bh_blk * g.NB + b) * D + c;
+      (which ? kmax : qmax)[o] = double(a);
+      (which ? kmin : qmin)[o] = double(z);
+      if (SICS) {
+        double u = 0.0;
+        for (int r = 0; r < G; ++r) u += upart[r][c];
+        u2 = u * u;
+      }
+    }
+    if (SICS) {
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) u2 += __shfl_xor(u2, m, 64);
+      if ((threadIdx.x & 63) == 0) sq[threadIdx.x >> 6] = u2;
+    }
+    __syncthreads();
+    if (SICS && threadIdx.x == 0) {
+      double t = 0.0;
+      for (int w = 0; w < D / 64; ++w) t += sq[w];
+      (which ? sics_k : sics_q)[bh_blk * g.NB + b] = t;
+    }
+    __syncthreads();
+  }
+}
+
+template <int D>
+hipError_t launch_mm(const DevGeom& g, const HeadMap& hm, const void* q, const void* k,
+                     double* qmax, double* qmin, double* kmax, double* kmin, double* sics_q,
+                     double* sics_k, hipStream_t s) {
+  const dim3 grid(g.NB, g.B * hm.n);
+  const uint4* q4 = static_cast<const uint4*>(q);
+  const uint4* k4 = static_cast<const uint4*>(k);
+  if (sics_q)
+    block_minmax_kernel<D, true><<<grid, kThreads, 0, s>>>(g, hm, q4, k4, qmax, qmin, kmax, kmin,
+                                                          sics_q, sics_k);
+  else
+    block_minmax_kernel<D, false><<<grid, kThreads, 0, s>>>(g, hm, q4, k4, qmax, qmin, kmax,
+                                                           kmin, nullptr, nullptr);
+  return hipGetLastError();
+}
+
 template <int D, bool SICS>
 hipError_t launch_bs(const DevGeom& g, const HeadMap& hm, const void* q, const void* k, void* qb,
                      void* kb, double* qbar, double* kbar, double* sics_q, double* sics_k,
@@ -310,6 +421,14 @@ hipError_t launch_block_summarize(const DevGeom& g, const HeadMap& hm, const voi
   if (g.d == 64)
     return sics_q ? launch_bs<64, true>(g, hm, q, k, qb, kb, qbar, kbar, sics_q, sics_k, s)
                   : launch_bs<64, false>(g, hm, q, k, qb, kb, qbar, kbar, nullptr, nullptr, s);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_block_minmax(const DevGeom& g, const HeadMap& hm, const void* q, const void* k,
+                               double* qmax, double* qmin, double* kmax, double* kmin,
+                               double* sics_q, double* sics_k, hipStream_t s) {
+  if (g.d == 128) return launch_mm<128>(g, hm, q, k, qmax, qmin, kmax, kmin, sics_q, sics_k, s);
+  if (g.d == 64) return launch_mm<64>(g, hm, q, k, qmax, qmin, kmax, kmin, sics_q, sics_k, s);
   return hipErrorInvalidValue;
 }
 

@@ -6,18 +6,47 @@ one fused call (spade_block_summarize, §3.3 optimisation (1)); `fused=False`
 issues spade_block_reorder x3 + spade_summarize instead. With `virtual=True`
 nothing is copied into the blocked layout: the summaries are read straight from
 the raster Q, K and the attention gathers its rows from, and writes O back to,
-the raster tensors (spade_sparse_attn_raster). All buffers are allocated once
+the raster tensors (spade_sparse_attn_raster). A `Scheme` selects the full mask
+composition instead of the plain Top-K/Top-P rule (spade_block_minmax for the
+DSA estimators' summaries, spade_compose_select). All buffers are allocated once
 here (torch, device memory); `run` only issues the library calls on one stream,
 with no host sync.
 """
 from __future__ import annotations
 
 import math
+from dataclasses import dataclass
 
 import numpy as np
 import torch
 
 from . import spade as S
+
+
+@dataclass
+class Scheme:
+    """One head-wise sparsity scheme (§3.1): estimator expression, inter-block
+    Top-K/Top-P value (optionally per head), intra-block filter, local-window
+    radii in blocks and attention-sink length in tokens."""
+    estimator: str = "mean"          # "mean" | "dsa" | "dsa2"
+    mode: str = "topk"               # "topk" | "topp"
+    topk: int = 1
+    tau: float = 1.0
+    topk_per_head: tuple | None = None
+    tau_per_head: tuple | None = None
+    intra: str | None = None         # None | "threshold" | "topk"
+    intra_theta: float = 0.0
+    intra_topk: int = 0
+    window: tuple = (-1, -1, -1)
+    sink: int = 0
+
+    @property
+    def extremes(self) -> bool:
+        return self.estimator != "mean"
+
+
+_EST = {"mean": S.SPADE_EST_MEAN, "dsa": S.SPADE_EST_DSA, "dsa2": S.SPADE_EST_DSA2}
+_INTRA = {None: S.SPADE_INTRA_NONE, "threshold": S.SPADE_INTRA_THRESHOLD, "topk": S.SPADE_INTRA_TOPK}
 
 
 def block_valid_counts(g) -> np.ndarray:
@@ -32,8 +61,12 @@ def block_valid_counts(g) -> np.ndarray:
 class SpadePath:
     def __init__(self, B, H, d, T, Hs, Ws, bt, bh, bw, *, mode="topp", topk=None, tau=None,
                  scale=None, device="cuda", with_sics=False, with_lse=False, fused=True,
-                 virtual=False):
+                 virtual=False, scheme: Scheme | None = None):
         self.g = S.geom(B, H, d, T, Hs, Ws, bt, bh, bw)
+        self.scheme = scheme
+        if scheme is not None:
+            mode, topk, tau = scheme.mode, scheme.topk, scheme.tau
+            with_sics = with_sics or scheme.intra is not None
         self.virtual = bool(virtual)
         self.fused = bool(fused) or self.virtual
         self._qkv = None
@@ -54,6 +87,22 @@ class SpadePath:
         self.kbar = torch.empty_like(self.qbar)
         self.sics_q = torch.empty((B, H, NB), dtype=torch.float64, device=dev) if with_sics else None
         self.sics_k = torch.empty_like(self.sics_q) if with_sics else None
+        self.ext = None  # (qmax, qmin, kmax, kmin) for the DSA estimators
+        self.spec = None
+        if scheme is not None:
+            if scheme.extremes:
+                self.ext = tuple(torch.empty((B, H, NB, d), dtype=torch.float64, device=dev)
+                                 for _ in range(4))
+            self._topk_h = (None if scheme.topk_per_head is None else
+                            torch.tensor(scheme.topk_per_head, dtype=torch.int32, device=dev))
+            self._tau_h = (None if scheme.tau_per_head is None else
+                           torch.tensor(scheme.tau_per_head, dtype=torch.float64, device=dev))
+            self.spec = S.mask_spec(_EST[scheme.estimator], self.mode, self.topk, self.tau,
+                                    self.scale, self._topk_h, self._tau_h, _INTRA[scheme.intra],
+                                    scheme.intra_topk, scheme.intra_theta, scheme.window,
+                                    scheme.sink)
+            self.summ = S.summaries(self.qbar, self.kbar, *(self.ext or (None,) * 4),
+                                    self.sics_q, self.sics_k)
         self.counts = torch.empty((B, H, NB), dtype=torch.int32, device=dev)
         self.indices = torch.empty((B, H, NB, NB), dtype=torch.int32, device=dev)
         lse_rows = g.N if self.virtual else NB * BS
@@ -65,6 +114,14 @@ class SpadePath:
     def reorder_in(self, Q, K, V, stream=None):
         """Blocking of Q, K, V; in fused mode also the summaries of Q and K; in
         virtual mode only the summaries (the raster tensors are kept for attend)."""
+        if self.ext is not None:  # DSA estimators: extremes (+ SICS) from the raster tensors
+            S.spade_block_minmax(self.g, Q, K, *self.ext, self.sics_q, self.sics_k, stream=stream)
+            if self.virtual:
+                self._qkv = (Q, K, V)
+                return
+            for x, y in ((Q, self.Qb), (K, self.Kb), (V, self.Vb)):
+                S.spade_block_reorder(self.g, x, y, inverse=False, stream=stream)
+            return
         if self.virtual:
             S.spade_block_summarize(self.g, Q, K, qbar=self.qbar, kbar=self.kbar,
                                     sics_q=self.sics_q, sics_k=self.sics_k, stream=stream)
@@ -80,12 +137,16 @@ class SpadePath:
 
     def summarize(self, stream=None):
         """Summaries of the blocked Q, K (already produced by reorder_in in fused mode)."""
-        if self.fused:
+        if self.fused or self.ext is not None:
             return
         S.spade_summarize(self.g, self.Qb, self.Kb, self.qbar, self.kbar, self.sics_q,
                           self.sics_k, stream=stream)
 
     def select(self, stream=None):
+        if self.spec is not None:
+            S.spade_compose_select(self.g, self.spec, self.summ, self.counts, self.indices,
+                                   stream=stream)
+            return
         S.spade_estimate_select(self.g, self.qbar, self.kbar, self.mode, self.topk, self.tau,
                                 self.scale, self.counts, self.indices, stream=stream)
 

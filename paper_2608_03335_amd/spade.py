@@ -17,10 +17,13 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspade.s
 SPADE_OK, SPADE_ERR_INVALID_ARG, SPADE_ERR_UNSUPPORTED, SPADE_ERR_WORKSPACE, SPADE_ERR_HIP = range(5)
 SPADE_BF16, SPADE_FP32 = 0, 1
 SPADE_TOPK, SPADE_TOPP = 0, 1
+SPADE_EST_MEAN, SPADE_EST_DSA, SPADE_EST_DSA2 = 0, 1, 2
+SPADE_INTRA_NONE, SPADE_INTRA_THRESHOLD, SPADE_INTRA_TOPK = 0, 1, 2
 
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_aggregation_score",
-            "spade_choose_scheme", "spade_estimate_select", "spade_attn_workspace_bytes",
+            "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
+            "spade_compose_select", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_sparse_attn_raster", "spade_status_string",
             "spade_last_error")
 MAX_HEAD_LIST = 64
@@ -52,6 +55,20 @@ def geom(B, H, d, T, Hs, Ws, bt, bh, bw) -> spade_geom:
     return spade_geom(B, H, d, T, Hs, Ws, bt, bh, bw)
 
 
+class spade_summaries(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("qbar", "kbar", "qmax", "qmin", "kmax", "kmin",
+                                               "sics_q", "sics_k")]
+
+
+class spade_mask_spec(ctypes.Structure):
+    _fields_ = [("estimator", ctypes.c_int32), ("mode", ctypes.c_int32), ("topk", ctypes.c_int32),
+                ("tau", ctypes.c_double), ("scale", ctypes.c_double),
+                ("topk_per_head", ctypes.c_void_p), ("tau_per_head", ctypes.c_void_p),
+                ("intra", ctypes.c_int32), ("intra_topk", ctypes.c_int32),
+                ("intra_theta", ctypes.c_double), ("window", ctypes.c_int32 * 3),
+                ("sink_tokens", ctypes.c_int64)]
+
+
 _lib = None
 
 
@@ -73,6 +90,10 @@ def lib() -> ctypes.CDLL:
             "spade_aggregation_score": (i32, [G, vp, vp, vp, vp, vp, vp]),
             "spade_choose_scheme": (i32, [vp, i32, i32, i32, vp, vp, vp]),
             "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
+            "spade_block_minmax": (i32, [G, vp, vp, vp, vp, vp, vp, vp, vp,
+                                         ctypes.POINTER(i32), i32, vp]),
+            "spade_compose_select": (i32, [G, ctypes.POINTER(spade_mask_spec),
+                                           ctypes.POINTER(spade_summaries), vp, vp, vp, vp]),
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
@@ -148,6 +169,38 @@ def spade_estimate_select(g: spade_geom, qbar, kbar, mode: int, topk: int, tau: 
     _check(lib().spade_estimate_select(ctypes.byref(g), _p(qbar), _p(kbar), int(mode), int(topk),
                                        float(tau), float(scale), _p(counts), _p(indices),
                                        _p(scores), _s(stream)))
+
+
+def spade_block_minmax(g: spade_geom, q, k, qmax, qmin, kmax, kmin, sics_q=None, sics_k=None,
+                       heads=None, stream=None):
+    arr, n = _head_list(heads)
+    _check(lib().spade_block_minmax(ctypes.byref(g), _p(q), _p(k), _p(qmax), _p(qmin), _p(kmax),
+                                    _p(kmin), _p(sics_q), _p(sics_k), arr, n, _s(stream)))
+
+
+def mask_spec(estimator=SPADE_EST_MEAN, mode=SPADE_TOPK, topk=0, tau=1.0, scale=1.0,
+              topk_per_head=None, tau_per_head=None, intra=SPADE_INTRA_NONE, intra_topk=0,
+              intra_theta=0.0, window=(-1, -1, -1), sink_tokens=0) -> spade_mask_spec:
+    """topk_per_head / tau_per_head: None or device tensors (int32 / fp64, [H]); the
+    caller keeps them alive until the call has run on its stream."""
+    return spade_mask_spec(int(estimator), int(mode), int(topk), float(tau), float(scale),
+                           None if topk_per_head is None else topk_per_head.data_ptr(),
+                           None if tau_per_head is None else tau_per_head.data_ptr(),
+                           int(intra), int(intra_topk), float(intra_theta),
+                           (ctypes.c_int32 * 3)(*[int(w) for w in window]), int(sink_tokens))
+
+
+def summaries(qbar=None, kbar=None, qmax=None, qmin=None, kmax=None, kmin=None, sics_q=None,
+              sics_k=None) -> spade_summaries:
+    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+    return spade_summaries(ptr(qbar), ptr(kbar), ptr(qmax), ptr(qmin), ptr(kmax), ptr(kmin),
+                           ptr(sics_q), ptr(sics_k))
+
+
+def spade_compose_select(g: spade_geom, spec: spade_mask_spec, summ: spade_summaries, counts,
+                         indices, scores=None, stream=None):
+    _check(lib().spade_compose_select(ctypes.byref(g), ctypes.byref(spec), ctypes.byref(summ),
+                                      _p(counts), _p(indices), _p(scores), _s(stream)))
 
 
 def spade_attn_workspace_bytes(g: spade_geom) -> int:

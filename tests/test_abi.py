@@ -216,3 +216,76 @@ def test_python_binding_raises_with_message():
     g = _g(d=96)
     with pytest.raises(S.SpadeError, match="head dim"):
         S._check(S.lib().spade_block_reorder(ctypes.byref(g), FAKE, FAKE, 0, 0, None, 0, None))
+
+
+def _summ(**kw):
+    f = dict(qbar=0x1000, kbar=0x1000, qmax=0x1000, qmin=0x1000, kmax=0x1000, kmin=0x1000,
+             sics_q=0x1000, sics_k=0x1000)
+    f.update(kw)
+    return S.spade_summaries(*[f[k] for k in ("qbar", "kbar", "qmax", "qmin", "kmax", "kmin",
+                                              "sics_q", "sics_k")])
+
+
+def _spec(**kw):
+    f = dict(estimator=S.SPADE_EST_DSA, mode=S.SPADE_TOPK, topk=4, tau=0.9, scale=0.1)
+    f.update(kw)
+    return S.mask_spec(**f)
+
+
+@pytest.mark.parametrize("spec,summ,expect", [
+    (dict(estimator=3), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(mode=2), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(topk=0), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(mode=S.SPADE_TOPP, tau=0.0), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(mode=S.SPADE_TOPP, tau=1.5), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(scale=0.0), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(intra=3), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(intra=S.SPADE_INTRA_TOPK, intra_topk=-1), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(intra=S.SPADE_INTRA_THRESHOLD, intra_theta=float("nan")), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(sink_tokens=-1), {}, S.SPADE_ERR_INVALID_ARG),
+    (dict(), dict(kmin=None), S.SPADE_ERR_INVALID_ARG),            # DSA needs max and min
+    (dict(estimator=S.SPADE_EST_MEAN), dict(qbar=None), S.SPADE_ERR_INVALID_ARG),
+    (dict(intra=S.SPADE_INTRA_THRESHOLD, intra_theta=0.5), dict(sics_k=None),
+     S.SPADE_ERR_INVALID_ARG),
+    (dict(), dict(qmax=0x1008), S.SPADE_ERR_INVALID_ARG),          # misaligned summary
+])
+def test_compose_select_errors(spec, summ, expect):
+    L = S.lib()
+    g = _g()
+    st = L.spade_compose_select(ctypes.byref(g), ctypes.byref(_spec(**spec)), ctypes.byref(_summ(**summ)),
+                                FAKE, FAKE, NULL, None)
+    assert st == expect, S.lib().spade_last_error().decode()
+
+
+def test_compose_select_null_structs_and_limits():
+    L = S.lib()
+    g = _g()
+    assert L.spade_compose_select(ctypes.byref(g), None, ctypes.byref(_summ()), FAKE, FAKE, NULL,
+                                  None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_compose_select(ctypes.byref(g), ctypes.byref(_spec()), None, FAKE, FAKE, NULL,
+                                  None) == S.SPADE_ERR_INVALID_ARG
+    assert L.spade_compose_select(ctypes.byref(g), ctypes.byref(_spec()), ctypes.byref(_summ()),
+                                  NULL, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG
+    big = _g(T=64, Hs=64, Ws=64, bt=2, bh=2, bw=4)               # NB = 32*32*16 > 1024
+    assert L.spade_compose_select(ctypes.byref(big), ctypes.byref(_spec()), ctypes.byref(_summ()),
+                                  FAKE, FAKE, NULL, None) == S.SPADE_ERR_UNSUPPORTED
+    empty = _g(B=0)
+    assert L.spade_compose_select(ctypes.byref(empty), ctypes.byref(_spec()), ctypes.byref(_summ()),
+                                  NULL, NULL, NULL, None) == S.SPADE_OK
+
+
+def test_block_minmax_errors():
+    L = S.lib()
+    g = _g()
+    args = [FAKE] * 6
+    assert L.spade_block_minmax(ctypes.byref(g), *args[:5], NULL, NULL, NULL, None, 0,
+                                None) == S.SPADE_ERR_INVALID_ARG     # kmin missing
+    assert L.spade_block_minmax(ctypes.byref(g), *args, FAKE, NULL, None, 0,
+                                None) == S.SPADE_ERR_INVALID_ARG     # one SICS output only
+    assert L.spade_block_minmax(ctypes.byref(g), MISALIGNED, *args[1:], NULL, NULL, None, 0,
+                                None) == S.SPADE_ERR_INVALID_ARG
+    bad = _heads(0, 0)
+    assert L.spade_block_minmax(ctypes.byref(g), *args, NULL, NULL, bad, 2,
+                                None) == S.SPADE_ERR_INVALID_ARG     # duplicate head
+    assert L.spade_block_minmax(ctypes.byref(_g(H=0)), NULL, NULL, NULL, NULL, NULL, NULL, NULL,
+                                NULL, None, 0, None) == S.SPADE_OK
