@@ -28,9 +28,10 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from gen.workloads import SWEEP_CANDIDATES, SWEEP_SPARSITIES, make_inputs, workload  # noqa: E402
+from gen.workloads import (DSA_SCHEMES, SWEEP_CANDIDATES, SWEEP_SPARSITIES, make_inputs,  # noqa: E402
+                           workload)
 from paper_2608_03335_amd import spade as S  # noqa: E402
-from paper_2608_03335_amd.pipeline import SpadePath, SweepPath, block_valid_counts  # noqa: E402
+from paper_2608_03335_amd.pipeline import Scheme, SpadePath, SweepPath, block_valid_counts  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
@@ -66,6 +67,11 @@ def stage_bytes(p: SpadePath, nvalid: np.ndarray) -> dict:
     N, NBS = g.N, g.NB * g.BS
     kept_entries = float(p.counts.sum().item())
     summaries = 2.0 * g.NB * d * 8
+    if p.ext is not None:
+        # extremes (4 fp64 [NB, d]) and SICS (2 fp64 [NB]) from the raster Q, K
+        ext = 4.0 * g.NB * d * 8 + 2.0 * g.NB * 8
+        return {"summaries": BH * (2.0 * N * row + ext),
+                "select": BH * (ext + g.NB * 4) + kept_entries * 4}
     if p.virtual:
         # summaries straight from the raster Q, K; nothing is blocked or restored
         return {"summaries": BH * (2.0 * N * row + summaries),
@@ -244,6 +250,10 @@ def main():
     ap.add_argument("--layout", default="raster", choices=["raster", "blocked"],
                     help="raster: attention gathers rows from the raster tensors (no blocked "
                          "copies); blocked: blocking + summaries pass, blocked attention, restore")
+    ap.add_argument("--scheme", default="plain", choices=["plain", "dsa"],
+                    help="plain: mean summaries + the workload's Top-K/Top-P rule; dsa: the "
+                         "full mask (DSA estimate, intra-block thresholding, inter Top-K, "
+                         "static window)")
     ap.add_argument("--sweep", action="store_true",
                     help="run the block-shape sweep (per-head blocking choice) instead")
     ap.add_argument("--copy-calib", action="store_true",
@@ -273,9 +283,17 @@ def main():
     cfg = workload(args.workload)
     log(f"workload {args.workload}: generating inputs on the GPU")
     Q, K, V = (x.to(torch.bfloat16) for x in make_inputs(cfg, seed=0, device=dev))
+    scheme, sel_label = None, cfg["mode"] + (f" tau={cfg['tau']}" if cfg["mode"] == "topp"
+                                             else f" k={cfg['topk']}")
+    if args.scheme == "dsa":
+        ds = DSA_SCHEMES[args.workload]
+        scheme = Scheme("dsa", "topk", topk=ds["topk"], intra="threshold",
+                        intra_theta=ds["intra_theta"], window=ds["window"])
+        sel_label = (f"dsa estimate, topk k={ds['topk']}, window {tuple(ds['window'])}, "
+                     f"intra coherence < {ds['intra_theta']}")
     p = SpadePath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"],
                   cfg["bh"], cfg["bw"], mode=cfg["mode"], topk=cfg.get("topk"),
-                  tau=cfg.get("tau"), device=dev, virtual=args.layout == "raster")
+                  tau=cfg.get("tau"), device=dev, virtual=args.layout == "raster", scheme=scheme)
     g = p.g
     nvalid_np = block_valid_counts(g)
     nvalid = torch.from_numpy(nvalid_np).to(dev)
@@ -382,8 +400,7 @@ def main():
         "config": {"workload": WORKLOAD_LABEL[args.workload], "layout": args.layout,
                    "B": g.B, "H": g.H, "d": g.d,
                    "grid": [g.T, g.Hs, g.Ws], "block": [g.bt, g.bh, g.bw], "N": g.N,
-                   "NB": g.NB, "selection": cfg["mode"] + (f" tau={cfg['tau']}" if cfg["mode"] == "topp"
-                                                            else f" k={cfg['topk']}"),
+                   "NB": g.NB, "selection": sel_label,
                    "block_sparsity": round(sparsity, 4),
                    "head_density_min_max": [round(float(dens_head.min()), 4),
                                             round(float(dens_head.max()), 4)]},

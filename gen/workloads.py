@@ -45,6 +45,18 @@ WORKLOADS = {
                           in_dtype="bf16"),
 }
 
+# The experiments' selection (DSA estimate, intra-block thresholding, inter Top-K)
+# plus a static spatial window, with budgets of roughly 80% dynamic and 20%
+# static blocks at about 85% block sparsity: k dynamic blocks per row and a
+# (0, 1, 1) window of up to 9 blocks. The coherence bound sits near the 1st
+# percentile of this generator's block coherence for the layer (seed 0), so the
+# filter marks about 1% of the blocks (mostly in the wide-field heads).
+DSA_SCHEMES = {
+    "hunyuan": dict(topk=43, window=(0, 1, 1), intra_theta=0.41),
+    "wan13b": dict(topk=27, window=(0, 1, 1), intra_theta=0.62),
+    "wan14b": dict(topk=76, window=(0, 1, 1), intra_theta=0.27),
+}
+
 # Blocking-scheme candidates of the block-shape sweep (two of 128 tokens, two
 # of 160) and its target block sparsities.
 SWEEP_CANDIDATES = ((2, 8, 8), (4, 4, 8), (4, 5, 8), (8, 5, 4))
