@@ -10,8 +10,8 @@
 // SICS is evaluated in the closed form |sum_k q_k/|q_k||^2, which equals the sum
 // of all pairwise cosines of Eq. (4) (expanding the square gives Eq. (5)'s
 // diagonal plus twice the off-diagonal sum, the quantity Alg. 1 accumulates).
-// It needs one row norm per token (a V-lane reduction) and no sequential scan,
-// so all rows of a block proceed in parallel.
+// It needs one row norm per token (a V-lane DPP reduction) and no sequential
+// scan, so all rows of a block proceed in parallel.
 #include "spade_internal.h"
 
 namespace spade {
@@ -28,6 +28,34 @@ __device__ __forceinline__ void bf16x8_to_f32(const uint4 v, float f[8]) {
   }
 }
 
+// One fp64 DPP step: v + (v of the lane that `ctrl` selects within the row).
+template <int CTRL>
+__device__ __forceinline__ double dpp_add(double v) {
+  const uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+  const int lo = __builtin_amdgcn_update_dpp(0, int(uint32_t(u)), CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, int(uint32_t(u >> 32)), CTRL, 0xf, 0xf, false);
+  return v + __longlong_as_double(static_cast<long long>((uint64_t(uint32_t(hi)) << 32) |
+                                                         uint32_t(lo)));
+}
+
+// Sum over each aligned group of V = 8 or 16 lanes (one token row), left in every
+// lane of the group: swap neighbours and pairs inside quads, then mirror the
+// half rows (quad 0 <-> 1, 2 <-> 3) and, for 16, the rows. All VALU (DPP), no LDS
+// round trips; partners add the same two values, so every lane gets the same bits.
+template <int V>
+__device__ __forceinline__ double row_group_sum(double v) {
+  v = dpp_add<0xB1>(v);   // quad_perm [1,0,3,2]
+  v = dpp_add<0x4E>(v);   // quad_perm [2,3,0,1]
+  v = dpp_add<0x141>(v);  // row_half_mirror
+  if (V == 16) v = dpp_add<0x140>(v);  // row_mirror
+  return v;
+}
+
+// Row loads in flight per lane: each lane loads its next kRowBatch rows before
+// reducing them (the rows a lane reduces, and their order, are those of a plain
+// loop over s = grp, grp + G, ...).
+constexpr int kRowBatch = 2;
+
 // 1/sqrt(x) for x > 0 in fp64: the hardware estimate (v_rsq_f64) refined by two
 // Newton steps y <- y (3 - x y^2) / 2, each of which squares the relative error;
 // much cheaper than a correctly rounded fp64 sqrt followed by a division.
@@ -37,6 +65,19 @@ __device__ __forceinline__ double inv_sqrt(double x) {
   y = y * (1.5 - hx * y * y);
   y = y * (1.5 - hx * y * y);
   return y;
+}
+
+// SICS accumulation of one token row held by V lanes (8 columns each): adds the
+// row's unit vector to uacc. A zero row adds exactly nothing.
+template <int V>
+__device__ __forceinline__ void add_unit_row(const float (&f)[8], double (&uacc)[8]) {
+  double ss = 0.0;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) ss += double(f[c]) * double(f[c]);
+  ss = row_group_sum<V>(ss);
+  const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
+#pragma unroll
+  for (int c = 0; c < 8; ++c) uacc[c] += double(f[c]) * inv;
 }
 
 template <int D, bool SICS>
@@ -63,21 +104,21 @@ __global__ void __launch_bounds__(kThreads) summarize_kernel(DevGeom g, const ui
     double acc[8], uacc[8];
 #pragma unroll
     for (int k = 0; k < 8; ++k) acc[k] = uacc[k] = 0.0;
-#pragma unroll 2
-    for (int s = grp; s < n; s += G) {
-      float f[8];
-      bf16x8_to_f32(src[int64_t(s) * V + vec], f);
+    for (int s0 = 0; s0 < n; s0 += kRowBatch * G) {  // zero rows past n add nothing
+      uint4 v[kRowBatch];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) acc[k] += double(f[k]);
-      if (SICS) {
-        double ss = 0.0;
+      for (int r = 0; r < kRowBatch; ++r) {
+        const int s = s0 + r * G + grp;
+        v[r] = make_uint4(0, 0, 0, 0);
+        if (s < n) v[r] = src[int64_t(s) * V + vec];
+      }
 #pragma unroll
-        for (int k = 0; k < 8; ++k) ss += double(f[k]) * double(f[k]);
+      for (int r = 0; r < kRowBatch; ++r) {
+        float f[8];
+        bf16x8_to_f32(v[r], f);
 #pragma unroll
-        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
-        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) uacc[k] += double(f[k]) * inv;
+        for (int k = 0; k < 8; ++k) acc[k] += double(f[k]);
+        if (SICS) add_unit_row<V>(f, uacc);
       }
     }
 #pragma unroll
@@ -145,24 +186,24 @@ __global__ void __launch_bounds__(kThreads) block_summarize_kernel(
     double acc[8], uacc[8];
 #pragma unroll
     for (int c = 0; c < 8; ++c) acc[c] = uacc[c] = 0.0;
-#pragma unroll 2
-    for (int s = grp; s < (WRITE ? g.BS : n); s += G) {
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (s < n) v = src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec];
-      if (WRITE) dst[int64_t(s) * V + vec] = v;
-      float f[8];
-      bf16x8_to_f32(v, f);  // padding rows are zero: they add nothing below
+    const int lim = WRITE ? g.BS : n;
+    for (int s0 = 0; s0 < lim; s0 += kRowBatch * G) {
+      uint4 v[kRowBatch];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) acc[c] += double(f[c]);
-      if (SICS) {
-        double ss = 0.0;
+      for (int r = 0; r < kRowBatch; ++r) {
+        const int s = s0 + r * G + grp;
+        v[r] = make_uint4(0, 0, 0, 0);
+        if (s < n) v[r] = src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec];
+      }
 #pragma unroll
-        for (int c = 0; c < 8; ++c) ss += double(f[c]) * double(f[c]);
+      for (int r = 0; r < kRowBatch; ++r) {
+        const int s = s0 + r * G + grp;
+        if (WRITE && s < lim) dst[int64_t(s) * V + vec] = v[r];
+        float f[8];
+        bf16x8_to_f32(v[r], f);  // padding rows are zero: they add nothing below
 #pragma unroll
-        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
-        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) uacc[c] += double(f[c]) * inv;
+        for (int c = 0; c < 8; ++c) acc[c] += double(f[c]);
+        if (SICS) add_unit_row<V>(f, uacc);
       }
     }
 #pragma unroll
@@ -234,24 +275,25 @@ __global__ void __launch_bounds__(kThreads) block_minmax_kernel(
       mn[c] = INFINITY;
       uacc[c] = 0.0;
     }
-#pragma unroll 2
-    for (int s = grp; s < n; s += G) {
-      float f[8];
-      bf16x8_to_f32(src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec], f);
+    for (int s0 = 0; s0 < n; s0 += kRowBatch * G) {
+      uint4 v[kRowBatch];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        mx[c] = fmaxf(mx[c], f[c]);
-        mn[c] = fminf(mn[c], f[c]);
+      for (int r = 0; r < kRowBatch; ++r) {
+        const int s = s0 + r * G + grp;
+        v[r] = make_uint4(0, 0, 0, 0);
+        if (s < n) v[r] = src[block_slot_token(g, e, r_ew, r_eh, s) * V + vec];
       }
-      if (SICS) {
-        double ss = 0.0;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) ss += double(f[c]) * double(f[c]);
+      for (int r = 0; r < kRowBatch; ++r) {
+        const bool real = s0 + r * G + grp < n;  // extremes skip the zero rows
+        float f[8];
+        bf16x8_to_f32(v[r], f);
 #pragma unroll
-        for (int m = 1; m < V; m <<= 1) ss += __shfl_xor(ss, m, V);
-        const double inv = ss > 0.0 ? inv_sqrt(ss) : 0.0;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) uacc[c] += double(f[c]) * inv;
+        for (int c = 0; c < 8; ++c) {
+          mx[c] = real ? fmaxf(mx[c], f[c]) : mx[c];
+          mn[c] = real ? fminf(mn[c], f[c]) : mn[c];
+        }
+        if (SICS) add_unit_row<V>(f, uacc);
       }
     }
 #pragma unroll
