@@ -64,6 +64,18 @@ tests pin them to the bounds they are built to be):
   * the mask is the OR of the inter Top-K/Top-P selection (computed on the inter
     scores alone) and the parts above; per-head k or tau values (the policy's
     head-wise budgets) replace the scalar ones.
+Readings of the policy function (§3.1 policy function; §4 configurations and the
+policy study), which the paper describes by its effect only:
+  * warm-up: the first ceil(0.30 n) denoising steps (text-to-video) or
+    ceil(0.25 n) (image-to-video) of n use full attention; Turbo only step 0;
+  * budget split: of k_total blocks per row, a static share (1/31 for Func 0,
+    whose dynamic:static budget is 30:1; 0.2 for Func 1, ~80% dynamic) goes to
+    the largest window of a fixed ladder of radii that fits in it; the dynamic
+    Top-K keeps the rest, k_dyn = k_total - window size;
+  * AS-guided budgets: head h gets k_h = clamp(floor(H k_dyn w_h / W + 1/2), 1, NB)
+    with w_h = 1 / AS_h (budget negatively correlated with the Selected
+    Aggregation Score; w_h = 0 when AS_h <= 0) and W the sum of the w_h in head
+    order (W = 0: every head gets clamp(k_dyn, 1, NB)).
 
 Every array here is float64 (inputs are upcast first). Shapes: Q, K, V are
 [B, H, N, d]; blocked tensors are [B, H, NB*BS, d].
@@ -630,6 +642,52 @@ def spade_attention_composed(Q, K, V, g: Geometry, spec: MaskSpec, scale=None) -
                                      r["indices"], g, scale)
     r.update(O=inverse_reorder(Ob, g), Ob=Ob, lse=lse)
     return r
+
+
+# --------------------------------------------------------------------------
+# Policy function (§3.1: head-wise sparsity-ratio schemes from the inference
+# state and the Selected Aggregation Score; §4: Func 0 / Func 1 budgets, dense
+# warm-up steps, Turbo)
+# --------------------------------------------------------------------------
+WINDOW_LADDER = ((0, 0, 0), (0, 0, 1), (0, 1, 1), (1, 1, 1), (1, 1, 2), (1, 2, 2), (2, 2, 2))
+STATIC_SHARE = {0: 1.0 / 31.0, 1: 0.2}
+
+
+def policy_dense(step: int, n_steps: int, task: str = "t2v", turbo: bool = False) -> bool:
+    """Whether denoising step `step` (0-based) of n_steps runs full attention."""
+    if turbo:
+        return step < 1
+    frac = 0.30 if task == "t2v" else 0.25
+    return step < int(np.ceil(frac * n_steps - 1e-9))
+
+
+def window_size(w) -> int:
+    return (2 * w[0] + 1) * (2 * w[1] + 1) * (2 * w[2] + 1)
+
+
+def policy_split(k_total: int, func: int):
+    """(window radii or None, window size, k_dyn) for a per-row budget of k_total."""
+    k_static = int(np.floor(k_total * STATIC_SHARE[func] + 0.5))
+    fits = [w for w in WINDOW_LADDER if window_size(w) <= k_static]
+    if not fits:
+        return None, 0, k_total
+    w = fits[-1]
+    return w, window_size(w), k_total - window_size(w)
+
+
+def policy_head_budgets(as_best, k_dyn: int, NB: int) -> np.ndarray:
+    """Per-head dynamic k, negatively correlated with the Selected AS (see header)."""
+    as_best = [float(a) for a in as_best]
+    H = len(as_best)
+    w = [1.0 / a if a > 0.0 else 0.0 for a in as_best]   # no score: no extra budget
+    W = 0.0
+    for x in w:                      # head order, one addition at a time
+        W += x
+    if not W > 0.0:                  # no head has a score: the flat budget
+        return np.full(H, min(max(k_dyn, 1), NB), dtype=np.int32)
+    total = float(H) * float(k_dyn)
+    return np.array([min(max(int(np.floor(total * x / W + 0.5)), 1), NB) for x in w],
+                    dtype=np.int32)
 
 
 # --------------------------------------------------------------------------

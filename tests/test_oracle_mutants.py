@@ -199,3 +199,23 @@ def test_key_marks_broadcast_along_rows_is_caught(monkeypatch):
                         lambda inter, iq=None, ik=None, w=None, s=None:
                         orig(inter, iq, None, w, s) | (ik[..., :, None] if ik is not None else False))
     assert _fails(TK.test_composition_is_the_or_of_its_parts)
+
+
+# ---- policy function ----
+from . import test_oracle_policy as TP  # noqa: E402
+
+
+def test_budgets_following_the_score_are_caught(monkeypatch):
+    orig = O.policy_head_budgets
+    monkeypatch.setattr(O, "policy_head_budgets",
+                        lambda a, kd, NB: orig([1.0 / x for x in a], kd, NB))
+    assert _fails(TP.test_budgets_fall_as_scores_rise_and_keep_the_total)
+
+
+def test_warmup_rounded_down_is_caught(monkeypatch):
+    def floor_warmup(step, n, task="t2v", turbo=False):
+        if turbo:
+            return step < 1
+        return step < int(np.floor((0.30 if task == "t2v" else 0.25) * n))
+    monkeypatch.setattr(O, "policy_dense", floor_warmup)
+    assert _fails(TP.test_dense_warmup_steps, 50, "i2v", False, 12)
