@@ -32,6 +32,7 @@ from gen.workloads import (DSA_SCHEMES, SWEEP_CANDIDATES, SWEEP_SPARSITIES, make
                            workload)
 from paper_2608_03335_amd import spade as S  # noqa: E402
 from paper_2608_03335_amd.pipeline import Scheme, SpadePath, SweepPath, block_valid_counts  # noqa: E402
+from paper_2608_03335_amd.policy import Policy  # noqa: E402
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
@@ -172,9 +173,10 @@ def sweep(args, dev):
     Q, K, V = (x.to(torch.bfloat16) for x in make_inputs(cfg, seed=0, device=dev))
     stream = torch.cuda.current_stream()
     rows = []
+    policy = None if args.policy == "none" else Policy(int(args.policy[-1]))
     for sp in SWEEP_SPARSITIES:
         p = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"],
-                      SWEEP_CANDIDATES, sp, device=dev)
+                      SWEEP_CANDIDATES, sp, device=dev, policy=policy)
         for _ in range(args.warmup):
             p.run(Q, K, V)
         torch.cuda.synchronize()
@@ -214,8 +216,11 @@ def sweep(args, dev):
             v = p.group_views(c, len(heads))
             nv = torch.from_numpy(block_valid_counts(v["g"])).to(dev)
             flops += kept_flops_lists(v["counts"], v["indices"], nv, cfg["d"])
+        kept = sum(float(p.group_views(c, len(h))["counts"].sum().item()) for c, h in p.work_list())
+        rows_total = sum(cfg["B"] * len(h) * p.geoms[c].NB ** 2 for c, h in p.work_list())
         sel = ms["evaluate"] + ms["group_select"]
         rows.append({
+            "block_sparsity": round(1.0 - kept / rows_total, 4),
             "target_block_sparsity": sp,
             "topk_per_candidate": dict(zip(["x".join(map(str, c)) for c in SWEEP_CANDIDATES], p.topk)),
             "heads_per_candidate": {"x".join(map(str, c)): len(hs) for c, hs in zip(SWEEP_CANDIDATES, groups)},
@@ -232,7 +237,10 @@ def sweep(args, dev):
                       "config": {"workload": "hunyuan-video-720p-61f attention layer (B1 H24 d128, "
                                              "grid 16x45x80), per-head choice among blocks "
                                              + ", ".join("x".join(map(str, c)) for c in SWEEP_CANDIDATES)
-                                             + ", top-k"},
+                                             + ", top-k"
+                                             + ("" if policy is None else
+                                                f", policy func {policy.func} (static window + "
+                                                "per-head k from the Selected AS)")},
                       "steps": args.steps, "warmup": args.warmup, "dtype": "bf16",
                       "data": "synthetic (seeded smooth-field + noise Q/K/V, per-head anisotropy)",
                       "sweep": rows, "device": torch.cuda.get_device_name(0)}))
@@ -254,6 +262,9 @@ def main():
                     help="plain: mean summaries + the workload's Top-K/Top-P rule; dsa: the "
                          "full mask (DSA estimate, intra-block thresholding, inter Top-K, "
                          "static window)")
+    ap.add_argument("--policy", default="none", choices=["none", "func0", "func1"],
+                    help="with --sweep: per-group budgets from the policy function (static "
+                         "window + per-head k inversely proportional to the Selected AS)")
     ap.add_argument("--sweep", action="store_true",
                     help="run the block-shape sweep (per-head blocking choice) instead")
     ap.add_argument("--copy-calib", action="store_true",

@@ -15,6 +15,8 @@
  *   spade_compose_select     the full mask: an estimator (mean, DSA, DSA2), the
  *                            Top-K/Top-P rule with optional per-head budgets, the
  *                            intra-block filter, local window and attention sink
+ *   spade_policy_budgets     per-head dynamic budgets from the Selected
+ *                            Aggregation Score (the policy function, §3.1)
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
@@ -275,6 +277,28 @@ typedef struct {
 spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* spec,
                                   const spade_summaries* sum, int32_t* counts, int32_t* indices,
                                   double* scores, hipStream_t stream);
+
+/*
+ * Head-wise budgets of the policy function — paper §3.1 (the policy function maps
+ * each head's Selected Aggregation Score and the inference state to its
+ * sparsity-ratio scheme) and §4 (the policy study: budgets negatively correlated
+ * with the score). The output feeds spade_mask_spec.topk_per_head.
+ *
+ *   as_best: fp64 [H] device: the Selected Aggregation Score per head (the `best`
+ *            output of spade_choose_scheme).
+ *   heads, n_heads: HOST list of heads as in spade_block_reorder (NULL: all H in
+ *            order); n = n_heads (H if NULL). Read before the call returns.
+ *   k_dyn:   mean dynamic blocks per row (>= 1); NB: upper clamp (>= 1).
+ *   k_out:   out, int32 [n] device, in list order:
+ *            k = clamp(floor(n * k_dyn * w / W + 1/2), 1, NB) with w = 1 / AS of the
+ *            head (0 when AS <= 0) and W the sum of the listed heads' w in list
+ *            order (W = 0: every head gets clamp(k_dyn, 1, NB)). fp64, correctly
+ *            rounded operations in a fixed order: the result is deterministic.
+ *   0 <= H <= 65535; H == 0 or an empty list is a no-op.
+ */
+spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_t* heads,
+                                  int32_t n_heads, int32_t k_dyn, int32_t NB, int32_t* k_out,
+                                  hipStream_t stream);
 
 /*
  * Scratch bytes spade_block_sparse_attn needs for its work schedule (the

@@ -16,7 +16,8 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libspade.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.cpp", "reorder.hip", "summarize.hip", "estimate_select.hip", "attn.hip"]
+SOURCES = ["api.cpp", "reorder.hip", "summarize.hip", "estimate_select.hip", "attn.hip",
+           "policy.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
           "-I", os.path.join(ROOT, "include"), "-I", CSRC,
           # keep the compiler from forming packed-fp32 VALU instructions

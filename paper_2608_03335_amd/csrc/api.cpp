@@ -295,6 +295,23 @@ spade_status spade_block_minmax(const spade_geom* g, const void* q, const void* 
                     "block_minmax launch");
 }
 
+spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_t* heads,
+                                  int32_t n_heads, int32_t k_dyn, int32_t NB, int32_t* k_out,
+                                  hipStream_t stream) {
+  if (H < 0 || H > 65535) return fail(SPADE_ERR_INVALID_ARG, "H must lie in [0, 65535] (got %d)", H);
+  if (k_dyn < 1) return fail(SPADE_ERR_INVALID_ARG, "k_dyn must be >= 1 (got %d)", k_dyn);
+  if (NB < 1) return fail(SPADE_ERR_INVALID_ARG, "NB must be >= 1 (got %d)", NB);
+  spade::DevGeom dg = {};
+  dg.H = H;
+  spade::HeadMap hm;
+  spade_status st = parse_heads(dg, heads, n_heads, &hm);
+  if (st != SPADE_OK) return st;
+  if (hm.n == 0) return SPADE_OK;
+  if (!as_best || !k_out) return fail(SPADE_ERR_INVALID_ARG, "as_best and k_out must be non-null");
+  return hip_status(spade::launch_policy_budgets(as_best, hm, k_dyn, NB, k_out, stream),
+                    "policy_budgets launch");
+}
+
 spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* spec,
                                   const spade_summaries* sum, int32_t* counts, int32_t* indices,
                                   double* scores, hipStream_t stream) {

@@ -111,6 +111,8 @@ struct SelectSpec {
   double* scores;
 };
 hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
+hipError_t launch_policy_budgets(const double* as_best, const HeadMap& hm, int k_dyn, int NB,
+                                 int* k_out, hipStream_t s);
 size_t attn_workspace_bytes(const DevGeom& g);
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,

@@ -45,6 +45,13 @@ class Scheme:
         return self.estimator != "mean"
 
 
+def _device_array(x, dtype, dev):
+    """None, a device tensor (used as is) or a sequence (copied to the device)."""
+    if x is None or isinstance(x, torch.Tensor):
+        return x
+    return torch.tensor(x, dtype=dtype, device=dev)
+
+
 _EST = {"mean": S.SPADE_EST_MEAN, "dsa": S.SPADE_EST_DSA, "dsa2": S.SPADE_EST_DSA2}
 _INTRA = {None: S.SPADE_INTRA_NONE, "threshold": S.SPADE_INTRA_THRESHOLD, "topk": S.SPADE_INTRA_TOPK}
 
@@ -93,10 +100,8 @@ class SpadePath:
             if scheme.extremes:
                 self.ext = tuple(torch.empty((B, H, NB, d), dtype=torch.float64, device=dev)
                                  for _ in range(4))
-            self._topk_h = (None if scheme.topk_per_head is None else
-                            torch.tensor(scheme.topk_per_head, dtype=torch.int32, device=dev))
-            self._tau_h = (None if scheme.tau_per_head is None else
-                           torch.tensor(scheme.tau_per_head, dtype=torch.float64, device=dev))
+            self._topk_h = _device_array(scheme.topk_per_head, torch.int32, dev)
+            self._tau_h = _device_array(scheme.tau_per_head, torch.float64, dev)
             self.spec = S.mask_spec(_EST[scheme.estimator], self.mode, self.topk, self.tau,
                                     self.scale, self._topk_h, self._tau_h, _INTRA[scheme.intra],
                                     scheme.intra_topk, scheme.intra_theta, scheme.window,
@@ -194,8 +199,10 @@ class SweepPath:
     blocking into the full output.
     """
 
-    def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda"):
+    def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda",
+                 policy=None):
         self.B, self.H, self.d = B, H, d
+        self.policy = policy  # None: uniform k per group; else the policy function's budgets
         self.shapes = [tuple(c) for c in candidates]
         self.sparsity = float(sparsity)
         self.scale = float(scale if scale is not None else 1.0 / math.sqrt(d))
@@ -224,7 +231,8 @@ class SweepPath:
                 qbar=torch.empty(B * cap * g.NB * d, dtype=f64, device=dev),
                 kbar=torch.empty(B * cap * g.NB * d, dtype=f64, device=dev),
                 counts=torch.empty(B * cap * g.NB, dtype=torch.int32, device=dev),
-                indices=torch.empty(B * cap * g.NB * g.NB, dtype=torch.int32, device=dev)))
+                indices=torch.empty(B * cap * g.NB * g.NB, dtype=torch.int32, device=dev),
+                k_heads=torch.empty(cap, dtype=torch.int32, device=dev)))
         self.ws = torch.empty(max(max(S.spade_attn_workspace_bytes(g) for g in self.geoms), 1),
                               dtype=torch.uint8, device=dev)
         self.O = torch.empty((B, H, T * Hs * Ws, d), dtype=bf, device=dev)
@@ -261,8 +269,18 @@ class SweepPath:
         S.spade_block_summarize(g, Q, K, v["Q"], v["K"], v["qbar"], v["kbar"], heads=heads,
                                 stream=stream)
         S.spade_block_reorder(g, V, v["V"], heads=heads, stream=stream)
-        S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
-                                self.scale, v["counts"], v["indices"], stream=stream)
+        if self.policy is None:
+            S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
+                                    self.scale, v["counts"], v["indices"], stream=stream)
+            return v
+        # the policy function: static window + per-head k from the Selected AS (§3.1)
+        kh = self.gb[c]["k_heads"][: len(heads)]
+        sc = self.policy.scheme(self.topk[c], g.NB, self.best, kh, heads=heads, stream=stream)
+        v["scheme"] = sc
+        spec = S.mask_spec(S.SPADE_EST_MEAN, S.SPADE_TOPK, sc.topk, 1.0, self.scale, kh, None,
+                           S.SPADE_INTRA_NONE, 0, 0.0, sc.window, 0)
+        S.spade_compose_select(v["g"], spec, S.summaries(v["qbar"], v["kbar"]), v["counts"],
+                               v["indices"], stream=stream)
         return v
 
     def group_attend(self, c, v, stream=None):

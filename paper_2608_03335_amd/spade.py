@@ -23,7 +23,7 @@ SPADE_INTRA_NONE, SPADE_INTRA_THRESHOLD, SPADE_INTRA_TOPK = 0, 1, 2
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
-            "spade_compose_select", "spade_attn_workspace_bytes",
+            "spade_compose_select", "spade_policy_budgets", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_sparse_attn_raster", "spade_status_string",
             "spade_last_error")
 MAX_HEAD_LIST = 64
@@ -94,6 +94,7 @@ def lib() -> ctypes.CDLL:
                                          ctypes.POINTER(i32), i32, vp]),
             "spade_compose_select": (i32, [G, ctypes.POINTER(spade_mask_spec),
                                            ctypes.POINTER(spade_summaries), vp, vp, vp, vp]),
+            "spade_policy_budgets": (i32, [vp, i32, ctypes.POINTER(i32), i32, i32, i32, vp, vp]),
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
@@ -201,6 +202,13 @@ def spade_compose_select(g: spade_geom, spec: spade_mask_spec, summ: spade_summa
                          indices, scores=None, stream=None):
     _check(lib().spade_compose_select(ctypes.byref(g), ctypes.byref(spec), ctypes.byref(summ),
                                       _p(counts), _p(indices), _p(scores), _s(stream)))
+
+
+def spade_policy_budgets(as_best, k_dyn: int, NB: int, k_out, heads=None, stream=None):
+    """as_best: fp64 [H] device tensor; k_out: int32 [len(heads) or H] device tensor."""
+    arr, n = _head_list(heads)
+    _check(lib().spade_policy_budgets(_p(as_best), int(as_best.numel()), arr, n, int(k_dyn),
+                                      int(NB), _p(k_out), _s(stream)))
 
 
 def spade_attn_workspace_bytes(g: spade_geom) -> int:

@@ -289,3 +289,15 @@ def test_block_minmax_errors():
                                 None) == S.SPADE_ERR_INVALID_ARG     # duplicate head
     assert L.spade_block_minmax(ctypes.byref(_g(H=0)), NULL, NULL, NULL, NULL, NULL, NULL, NULL,
                                 NULL, None, 0, None) == S.SPADE_OK
+
+
+def test_policy_budgets_errors():
+    L = S.lib()
+    ok = L.spade_policy_budgets
+    assert ok(FAKE, -1, None, 0, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG      # negative H
+    assert ok(FAKE, 4, None, 0, 0, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG       # k_dyn < 1
+    assert ok(FAKE, 4, None, 0, 4, 0, FAKE, None) == S.SPADE_ERR_INVALID_ARG        # NB < 1
+    assert ok(NULL, 4, None, 0, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG       # null input
+    assert ok(FAKE, 4, _heads(0, 4), 2, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG  # head 4 >= H
+    assert ok(FAKE, 4, _heads(1, 1), 2, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG  # duplicate
+    assert ok(NULL, 0, None, 0, 4, 10, NULL, None) == S.SPADE_OK                     # H = 0: no-op
