@@ -176,7 +176,8 @@ def sweep(args, dev):
     policy = None if args.policy == "none" else Policy(int(args.policy[-1]))
     for sp in SWEEP_SPARSITIES:
         p = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"],
-                      SWEEP_CANDIDATES, sp, device=dev, policy=policy)
+                      SWEEP_CANDIDATES, sp, device=dev, policy=policy,
+                      raster=args.layout == "raster")
         for _ in range(args.warmup):
             p.run(Q, K, V)
         torch.cuda.synchronize()
@@ -190,7 +191,16 @@ def sweep(args, dev):
             e[1].record(stream)
             work = p.work_list(stream)          # host read of the per-head choice
             marks = []
-            for c, heads in work:
+            if p.raster:  # group summaries + lists, then one multi-scheme attention call
+                m = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+                m[0].record(stream)
+                selected = [(c, heads, p.group_select(c, heads, Q, K, V)) for c, heads in work]
+                m[1].record(stream)
+                p.attend_all(selected, Q, K, V)
+                m[2].record(stream)
+                m[3].record(stream)
+                marks.append((None, None, None, m))
+            for c, heads in ([] if p.raster else work):
                 m = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
                 m[0].record(stream)
                 v = p.group_select(c, heads, Q, K, V)
@@ -234,6 +244,7 @@ def sweep(args, dev):
         del p
         torch.cuda.empty_cache()
     print(json.dumps({"metric": "block-shape sweep: selection-stage time / attention time",
+                      "layout": args.layout,
                       "config": {"workload": "hunyuan-video-720p-61f attention layer (B1 H24 d128, "
                                              "grid 16x45x80), per-head choice among blocks "
                                              + ", ".join("x".join(map(str, c)) for c in SWEEP_CANDIDATES)

@@ -19,6 +19,7 @@
  *                            Aggregation Score (the policy function, §3.1)
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
+ *   spade_sparse_attn_raster_multi  the same over heads with different blockings
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
  *   spade_aggregation_score  per-head Aggregation Score of one candidate scheme
  *   spade_choose_scheme      per-head argmax over the candidates
@@ -350,6 +351,38 @@ spade_status spade_sparse_attn_raster(const spade_geom* g, const void* q, const 
                                       const int32_t* indices, double scale, void* o, float* lse,
                                       void* workspace, size_t workspace_bytes,
                                       hipStream_t stream);
+
+/* Block lists of one head for spade_sparse_attn_raster_multi (device pointers). */
+typedef struct {
+  int32_t scheme;           /* index of the head's blocking among the call's geometries */
+  const int32_t* counts;    /* counts of (batch 0, this head): [NB] of its blocking */
+  const int32_t* indices;   /* kept lists of (batch 0, this head): [NB, NB] */
+  int64_t counts_bstride;   /* elements from one batch element's counts to the next */
+  int64_t indices_bstride;  /* elements from one batch element's lists to the next */
+} spade_head_lists;
+
+/*
+ * Head-wise sparse attention over heads with different blockings — paper §3.2
+ * (each head runs under its own Selected Blocking Scheme) and §3.3 (2) (heads
+ * sharing work are launched together): the raster attention of
+ * spade_sparse_attn_raster for every head in one pass over the shared raster
+ * Q, K, V, each head addressed through its own blocking.
+ *
+ *   geoms, n_geoms: the candidate blockings (1 <= n_geoms <= 8); all must share B,
+ *            H, d and the grid (T, Hs, Ws). H <= 64.
+ *   heads:   HOST array [H]: per head its blocking and block lists (any layout, e.g.
+ *            per-group buffers written by spade_compose_select with a head list).
+ *   q, k, v, scale, o, lse, workspace: as for spade_sparse_attn_raster.
+ *   Each head's output equals spade_sparse_attn_raster's under its own blocking,
+ *   bit for bit. Heads whose blocks need the same number of 32-row waves
+ *   (ceil(BS/32)) run in one launch: one launch in total when all blockings
+ *   share it.
+ */
+spade_status spade_sparse_attn_raster_multi(const spade_geom* geoms, int32_t n_geoms,
+                                            const spade_head_lists* heads, const void* q,
+                                            const void* k, const void* v, double scale, void* o,
+                                            float* lse, void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char* spade_status_string(spade_status s);

@@ -295,6 +295,63 @@ spade_status spade_block_minmax(const spade_geom* g, const void* q, const void* 
                     "block_minmax launch");
 }
 
+spade_status spade_sparse_attn_raster_multi(const spade_geom* geoms, int32_t n_geoms,
+                                            const spade_head_lists* heads, const void* q,
+                                            const void* k, const void* v, double scale, void* o,
+                                            float* lse, void* workspace, size_t workspace_bytes,
+                                            hipStream_t stream) {
+  if (!geoms || n_geoms < 1 || n_geoms > spade::kMaxMultiGeoms)
+    return fail(SPADE_ERR_INVALID_ARG, "need 1..%d geometries (got %d)", spade::kMaxMultiGeoms,
+                n_geoms);
+  spade::DevGeom dg[spade::kMaxMultiGeoms];
+  bool empty = false;
+  for (int c = 0; c < n_geoms; ++c) {
+    bool e = false;
+    spade_status st = check_geom(&geoms[c], &dg[c], &e);
+    if (st != SPADE_OK) return st;
+    const spade_geom& a = geoms[0];
+    const spade_geom& b = geoms[c];
+    if (b.B != a.B || b.H != a.H || b.d != a.d || b.T != a.T || b.Hs != a.Hs || b.Ws != a.Ws)
+      return fail(SPADE_ERR_INVALID_ARG, "geometry %d differs from geometry 0 outside the blocking",
+                  c);
+    empty = e;
+    if (!e && dg[c].NB > spade::kMaxAttnNB)
+      return fail(SPADE_ERR_UNSUPPORTED, "NB=%d exceeds the attention limit %d", dg[c].NB,
+                  spade::kMaxAttnNB);
+  }
+  if (!(isfinite(scale) && scale > 0.0))
+    return fail(SPADE_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", scale);
+  if (dg[0].H > spade::kMaxMultiHeads)
+    return fail(SPADE_ERR_UNSUPPORTED, "H=%d exceeds %d heads per call", dg[0].H,
+                spade::kMaxMultiHeads);
+  if (!empty && dg[0].N * int64_t(dg[0].d) * 2 >= (int64_t(1) << 31))
+    return fail(SPADE_ERR_UNSUPPORTED, "raster attention needs N*d*2 < 2^31 bytes per head");
+  if (empty) return SPADE_OK;
+  if (!heads) return fail(SPADE_ERR_INVALID_ARG, "heads must be non-null");
+  if (!q || !k || !v || !o) return fail(SPADE_ERR_INVALID_ARG, "q, k, v and o must be non-null");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
+  spade::MultiHead mh[spade::kMaxMultiHeads];
+  for (int h = 0; h < dg[0].H; ++h) {
+    const spade_head_lists& x = heads[h];
+    if (x.scheme < 0 || x.scheme >= n_geoms)
+      return fail(SPADE_ERR_INVALID_ARG, "heads[%d].scheme=%d outside [0, %d)", h, x.scheme,
+                  n_geoms);
+    if (!x.counts || !x.indices)
+      return fail(SPADE_ERR_INVALID_ARG, "heads[%d]: counts and indices must be non-null", h);
+    if (x.counts_bstride < 0 || x.counts_bstride >= (int64_t(1) << 31) || x.indices_bstride < 0)
+      return fail(SPADE_ERR_INVALID_ARG, "heads[%d]: batch strides out of range", h);
+    mh[h] = {x.counts, x.indices, x.indices_bstride, int(x.counts_bstride), x.scheme, h, 0};
+  }
+  const size_t need = spade::attn_workspace_bytes(dg[0]);
+  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
+    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                workspace_bytes);
+  return hip_status(spade::launch_sparse_attn_multi(dg, n_geoms, mh, dg[0].H, q, k, v,
+                                                    float(scale), o, lse, stream),
+                    "multi-scheme attention launch");
+}
+
 spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_t* heads,
                                   int32_t n_heads, int32_t k_dyn, int32_t NB, int32_t* k_out,
                                   hipStream_t stream) {

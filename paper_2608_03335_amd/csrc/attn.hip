@@ -30,6 +30,8 @@
 // raised (and O rescaled) when some row's max grows by more than 2^8, so most
 // chunks skip the 64-register rescale; row sums use bf16 dot2 on the same packed
 // P that feeds the MFMA.
+#include <type_traits>
+
 #include "spade_internal.h"
 
 namespace spade {
@@ -225,13 +227,18 @@ __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, c
 // 5 compute waves with one (2 workgroups of 6).
 // RASTER: q, k, v and o are raster [B,H,N,d] (and lse [B,H,N]); every row is
 // addressed through the blocking's slot -> token map, so no blocked copies exist.
-template <int D, int W, bool LD, bool RASTER>
+struct NoTable {};
+
+// MULTI (raster only): one launch over heads with different blockings; the work
+// item picks its head, and with it the geometry and block lists, from `tab`.
+template <int D, int W, bool LD, bool RASTER, bool MULTI>
 __global__ void __launch_bounds__(64 * (W + LD))
     __attribute__((amdgpu_waves_per_eu(W + LD >= 3 ? 3 : 2)))
-    attn_kernel(DevGeom g, const uint4* __restrict__ qb, const char* __restrict__ kb,
+    attn_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
                 const char* __restrict__ vb, const int* __restrict__ counts,
                 const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
-                float* __restrict__ lse) {
+                float* __restrict__ lse,
+                typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
   using TL = Tile<D>;
   __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
   __shared__ int rel_raw[RASTER ? kMaxBS : 1];  // full-block slot -> raster token offset
@@ -244,11 +251,36 @@ __global__ void __launch_bounds__(64 * (W + LD))
   // and takes one contiguous eighth of each head's query blocks: the XCDs work
   // on the same head at a time (its K/V stays in the MALL) and each XCD's L2
   // serves spatially adjacent query blocks, whose kept K/V sets overlap.
-  const int per_xcd = (g.NB + 7) / 8;
-  const int64_t slot = int64_t(blockIdx.x) >> 3;
-  const int64_t bh = slot / per_xcd;
-  const int i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
-  if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
+  // MULTI: the heads follow each other in the grid (per batch element), each
+  // padded to a multiple of 8 items, and are dealt to the XCDs the same way.
+  DevGeom g = g_arg;
+  int64_t bh;
+  int i;
+  const int* cnt_src;
+  const int* list_src;
+  if constexpr (MULTI) {
+    const int b = int(blockIdx.x) / tab.items_per_batch;
+    const int w = int(blockIdx.x) - b * tab.items_per_batch;
+    int k = 0;
+    while (k + 1 < tab.n_heads && tab.head[k + 1].start <= w) ++k;
+    const MultiHead& mh = tab.head[k];
+    g = tab.geo[mh.geom];
+    const int local = w - mh.start;  // same residue mod 8 as blockIdx.x
+    const int per_xcd = (g.NB + 7) / 8;
+    i = (local & 7) * per_xcd + (local >> 3);
+    if (i >= g.NB) return;
+    bh = int64_t(b) * g.H + mh.h;
+    cnt_src = mh.counts + int64_t(b) * mh.counts_bstride + i;
+    list_src = mh.indices + int64_t(b) * mh.indices_bstride + int64_t(i) * g.NB;
+  } else {
+    const int per_xcd = (g.NB + 7) / 8;
+    const int64_t slot = int64_t(blockIdx.x) >> 3;
+    bh = slot / per_xcd;
+    i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
+    if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
+    cnt_src = counts + bh * g.NB + i;
+    list_src = indices + (bh * g.NB + i) * int64_t(g.NB);
+  }
   const BlockExt e_i = block_ext(g, i);
   const int n_i = e_i.n;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -276,11 +308,8 @@ __global__ void __launch_bounds__(64 * (W + LD))
     }
   }
 
-  const int cnt = min(max(counts[bh * g.NB + i], 0), g.NB);
-  {
-    const int* src = indices + (bh * g.NB + i) * int64_t(g.NB);
-    for (int e = threadIdx.x; e < cnt; e += 64 * (W + LD)) list[e] = src[e];
-  }
+  const int cnt = min(max(*cnt_src, 0), g.NB);
+  for (int e = threadIdx.x; e < cnt; e += 64 * (W + LD)) list[e] = list_src[e];
   if (RASTER) {
     for (int sl = threadIdx.x; sl < g.BS; sl += 64 * (W + LD)) {
       const int q = sl / g.bw;
@@ -471,32 +500,46 @@ __global__ void __launch_bounds__(64 * (W + LD))
   }
 }
 
-template <int D, int W, bool LD, bool RASTER>
+template <int D, int W, bool LD, bool RASTER, bool MULTI>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
-                     hipStream_t s) {
-  const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
+                     hipStream_t s, const MultiTable* tab = nullptr) {
   static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<D, W, LD, RASTER>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       int(kMaxAttnNB * sizeof(int)));
+    hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&attn_kernel<D, W, LD, RASTER, MULTI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, int(kMaxAttnNB * sizeof(int)));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
-  attn_kernel<D, W, LD, RASTER><<<dim3(unsigned(items)), 64 * (W + LD), size_t(g.NB) * sizeof(int),
-                                  s>>>(
-      g, static_cast<const uint4*>(qb), static_cast<const char*>(kb),
-      static_cast<const char*>(vb), counts, indices, scale_log2, static_cast<__bf16*>(ob), lse);
+  const uint4* q4 = static_cast<const uint4*>(qb);
+  const char* k1 = static_cast<const char*>(kb);
+  const char* v1 = static_cast<const char*>(vb);
+  __bf16* o2 = static_cast<__bf16*>(ob);
+  if constexpr (MULTI) {
+    int nb_max = 0;
+    for (int k = 0; k < tab->n_heads; ++k) nb_max = max(nb_max, tab->geo[tab->head[k].geom].NB);
+    const int64_t items = int64_t(g.B) * tab->items_per_batch;
+    attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
+                                           size_t(nb_max) * sizeof(int), s>>>(
+        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, *tab);
+  } else {
+    const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
+    attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
+                                           size_t(g.NB) * sizeof(int), s>>>(
+        g, q4, k1, v1, counts, indices, scale_log2, o2, lse, NoTable{});
+  }
   return hipGetLastError();
 }
 
-template <int D, bool RASTER>
+template <int D, bool RASTER, bool MULTI = false>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
-                    hipStream_t s) {
-#define SPADE_ATTN_CASE(w, ld) \
-  case w: return launch_dw<D, w, ld, RASTER>(g, qb, kb, vb, counts, indices, scale_log2, ob, lse, s);
+                    hipStream_t s, const MultiTable* tab = nullptr) {
+#define SPADE_ATTN_CASE(w, ld)                                                                  \
+  case w:                                                                                       \
+    return launch_dw<D, w, ld, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob, \
+                                              lse, s, tab);
   // loader wave unless it would cost a workgroup per CU (4 or 6 compute waves)
   switch ((g.BS + 31) / 32) {
     SPADE_ATTN_CASE(1, true) SPADE_ATTN_CASE(2, true) SPADE_ATTN_CASE(3, true)
@@ -510,6 +553,35 @@ hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void
 }  // namespace
 
 size_t attn_workspace_bytes(const DevGeom&) { return 0; }
+
+hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHead* heads,
+                                    int n_heads, const void* q, const void* k, const void* v,
+                                    float scale, void* o, float* lse, hipStream_t s) {
+  const float sl2 = scale * 1.44269504088896340736f;
+  // one launch per workgroup shape; the launch's geometry carries that shape's BS
+  for (int w = 1; w <= kMaxBS / 32; ++w) {
+    MultiTable tab = {};
+    for (int c = 0; c < n_geo; ++c) tab.geo[c] = geo[c];
+    int start = 0, widest = -1;
+    for (int hh = 0; hh < n_heads; ++hh) {
+      const DevGeom& gh = geo[heads[hh].geom];
+      if ((gh.BS + 31) / 32 != w) continue;
+      MultiHead mh = heads[hh];
+      mh.start = start;
+      start += (gh.NB + 7) / 8 * 8;
+      tab.head[tab.n_heads++] = mh;
+      if (widest < 0 || gh.BS > geo[widest].BS) widest = heads[hh].geom;
+    }
+    if (tab.n_heads == 0) continue;
+    tab.items_per_batch = start;
+    const DevGeom& gl = geo[widest];
+    const hipError_t e = gl.d == 128
+        ? launch_d<128, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab)
+        : launch_d<64, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,

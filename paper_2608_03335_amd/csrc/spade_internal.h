@@ -114,6 +114,30 @@ hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
 hipError_t launch_policy_budgets(const double* as_best, const HeadMap& hm, int k_dyn, int NB,
                                  int* k_out, hipStream_t s);
 size_t attn_workspace_bytes(const DevGeom& g);
+// One attention launch over heads with different blockings (one grid, one shared
+// raster Q/K/V): per head its geometry, its block lists and its first work item.
+constexpr int kMaxMultiGeoms = 8;
+constexpr int kMaxMultiHeads = 64;
+struct MultiHead {
+  const int* counts;        // (batch 0, this head): [NB]
+  const int* indices;       // (batch 0, this head): [NB, NB]
+  int64_t indices_bstride;  // elements between batch elements
+  int counts_bstride;
+  int geom;                 // index into MultiTable::geo
+  int h;                    // raster head index
+  int start;                // first work item of the head in each batch element
+};
+struct MultiTable {
+  DevGeom geo[kMaxMultiGeoms];
+  MultiHead head[kMaxMultiHeads];
+  int n_heads;              // heads of this launch, in ascending `start`
+  int items_per_batch;      // work items per batch element (a multiple of 8)
+};
+// One launch per distinct workgroup shape (compute waves = ceil(BS / 32)); heads
+// whose blockings share a shape run in the same launch.
+hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHead* heads,
+                                    int n_heads, const void* q, const void* k, const void* v,
+                                    float scale, void* o, float* lse, hipStream_t s);
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,
                                     float scale, void* ob, float* lse, void* ws, bool raster,

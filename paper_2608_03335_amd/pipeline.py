@@ -196,12 +196,18 @@ class SweepPath:
     group then runs the fused blocking + summaries of Q, K with its head list
     (§3.3 (1), (2)), the blocking of V, Top-K selection with
     k = max(1, round((1 - s) NB)), block-sparse attention and the inverse
-    blocking into the full output.
+    blocking into the full output. With `raster=True` (at most 64 heads) the
+    groups compute only their summaries and block lists, and one multi-scheme
+    call (spade_sparse_attn_raster_multi) attends every head from the raster
+    tensors under its own blocking and writes O in raster order.
     """
 
     def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda",
-                 policy=None):
+                 policy=None, raster=False):
         self.B, self.H, self.d = B, H, d
+        self.raster = bool(raster)
+        if self.raster and H > S.MAX_HEAD_LIST:
+            raise ValueError(f"raster sweep supports at most {S.MAX_HEAD_LIST} heads")
         self.policy = policy  # None: uniform k per group; else the policy function's budgets
         self.shapes = [tuple(c) for c in candidates]
         self.sparsity = float(sparsity)
@@ -222,7 +228,7 @@ class SweepPath:
         cap = min(H, S.MAX_HEAD_LIST)
         self.gb = []
         for g in self.geoms:
-            rows = g.NB * g.BS
+            rows = 0 if self.raster else g.NB * g.BS  # the raster sweep blocks nothing
             self.gb.append(dict(
                 Q=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
                 K=torch.empty(B * cap * rows * d, dtype=bf, device=dev),
@@ -255,8 +261,9 @@ class SweepPath:
         gg = S.geom(self.B, n, self.d, g.T, g.Hs, g.Ws, g.bt, g.bh, g.bw)
         b, rows, NB = self.gb[c], g.NB * g.BS, g.NB
         v = dict(g=gg)
-        for k in ("Q", "K", "V", "O"):
-            v[k] = b[k][: self.B * n * rows * self.d].view(self.B, n, rows, self.d)
+        for k in ("Q", "K", "V", "O"):  # blocked group tensors (none in raster mode)
+            v[k] = None if self.raster else b[k][: self.B * n * rows * self.d].view(
+                self.B, n, rows, self.d)
         for k in ("qbar", "kbar"):
             v[k] = b[k][: self.B * n * NB * self.d].view(self.B, n, NB, self.d)
         v["counts"] = b["counts"][: self.B * n * NB].view(self.B, n, NB)
@@ -266,9 +273,13 @@ class SweepPath:
     # group stages, separately callable so they can be timed
     def group_select(self, c, heads, Q, K, V, stream=None):
         g, v = self.geoms[c], self.group_views(c, len(heads))
-        S.spade_block_summarize(g, Q, K, v["Q"], v["K"], v["qbar"], v["kbar"], heads=heads,
-                                stream=stream)
-        S.spade_block_reorder(g, V, v["V"], heads=heads, stream=stream)
+        if self.raster:
+            S.spade_block_summarize(g, Q, K, qbar=v["qbar"], kbar=v["kbar"], heads=heads,
+                                    stream=stream)
+        else:
+            S.spade_block_summarize(g, Q, K, v["Q"], v["K"], v["qbar"], v["kbar"], heads=heads,
+                                    stream=stream)
+            S.spade_block_reorder(g, V, v["V"], heads=heads, stream=stream)
         if self.policy is None:
             S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
                                     self.scale, v["counts"], v["indices"], stream=stream)
@@ -291,6 +302,17 @@ class SweepPath:
         S.spade_block_reorder(self.geoms[c], v["O"], self.O, inverse=True, heads=heads,
                               stream=stream)
 
+    def attend_all(self, selected, Q, K, V, stream=None):
+        """Raster mode: one multi-scheme call over every head; `selected` holds the
+        (candidate, heads, views) of each group."""
+        table = [None] * self.H
+        for c, heads, v in selected:
+            NB, n = self.geoms[c].NB, len(heads)
+            for k, h in enumerate(heads):
+                table[h] = (c, v["counts"][0, k], v["indices"][0, k], n * NB, n * NB * NB)
+        S.spade_sparse_attn_raster_multi(self.geoms, table, Q, K, V, self.scale, self.O,
+                                         workspace=self.ws, stream=stream)
+
     def work_list(self, stream=None):
         """[(candidate, heads)] with every group split into chunks of <= 64 heads."""
         return [(c, hs) for c, grp in enumerate(self.groups(stream))
@@ -298,6 +320,11 @@ class SweepPath:
 
     def run(self, Q, K, V, stream=None):
         self.evaluate(Q, K, stream)
+        if self.raster:
+            selected = [(c, heads, self.group_select(c, heads, Q, K, V, stream))
+                        for c, heads in self.work_list(stream)]
+            self.attend_all(selected, Q, K, V, stream)
+            return self.O
         for c, heads in self.work_list(stream):
             v = self.group_select(c, heads, Q, K, V, stream)
             self.group_attend(c, v, stream)

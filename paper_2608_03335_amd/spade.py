@@ -24,7 +24,8 @@ EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
             "spade_compose_select", "spade_policy_budgets", "spade_attn_workspace_bytes",
-            "spade_block_sparse_attn", "spade_sparse_attn_raster", "spade_status_string",
+            "spade_block_sparse_attn", "spade_sparse_attn_raster",
+            "spade_sparse_attn_raster_multi", "spade_status_string",
             "spade_last_error")
 MAX_HEAD_LIST = 64
 
@@ -53,6 +54,12 @@ class spade_geom(ctypes.Structure):
 
 def geom(B, H, d, T, Hs, Ws, bt, bh, bw) -> spade_geom:
     return spade_geom(B, H, d, T, Hs, Ws, bt, bh, bw)
+
+
+class spade_head_lists(ctypes.Structure):
+    _fields_ = [("scheme", ctypes.c_int32), ("counts", ctypes.c_void_p),
+                ("indices", ctypes.c_void_p), ("counts_bstride", ctypes.c_int64),
+                ("indices_bstride", ctypes.c_int64)]
 
 
 class spade_summaries(ctypes.Structure):
@@ -98,6 +105,8 @@ def lib() -> ctypes.CDLL:
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
+            "spade_sparse_attn_raster_multi": (i32, [G, i32, ctypes.POINTER(spade_head_lists), vp,
+                                                     vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_status_string": (ctypes.c_char_p, [i32]),
             "spade_last_error": (ctypes.c_char_p, []),
         }
@@ -202,6 +211,21 @@ def spade_compose_select(g: spade_geom, spec: spade_mask_spec, summ: spade_summa
                          indices, scores=None, stream=None):
     _check(lib().spade_compose_select(ctypes.byref(g), ctypes.byref(spec), ctypes.byref(summ),
                                       _p(counts), _p(indices), _p(scores), _s(stream)))
+
+
+def spade_sparse_attn_raster_multi(geoms, heads, q, k, v, scale: float, o, lse=None,
+                                   workspace=None, stream=None):
+    """geoms: sequence of spade_geom; heads: per head (scheme, counts, indices,
+    counts_bstride, indices_bstride) with counts/indices device tensors (views at
+    batch 0 of the head)."""
+    ga = (spade_geom * len(geoms))(*geoms)
+    ha = (spade_head_lists * max(len(heads), 1))(
+        *[spade_head_lists(int(c), cn.data_ptr(), ix.data_ptr(), int(cs), int(xs))
+          for c, cn, ix, cs, xs in heads])
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().spade_sparse_attn_raster_multi(ga, len(geoms), ha, _p(q), _p(k), _p(v),
+                                                float(scale), _p(o), _p(lse), _p(workspace),
+                                                nbytes, _s(stream)))
 
 
 def spade_policy_budgets(as_best, k_dyn: int, NB: int, k_out, heads=None, stream=None):

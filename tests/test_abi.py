@@ -301,3 +301,29 @@ def test_policy_budgets_errors():
     assert ok(FAKE, 4, _heads(0, 4), 2, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG  # head 4 >= H
     assert ok(FAKE, 4, _heads(1, 1), 2, 4, 10, FAKE, None) == S.SPADE_ERR_INVALID_ARG  # duplicate
     assert ok(NULL, 0, None, 0, 4, 10, NULL, None) == S.SPADE_OK                     # H = 0: no-op
+
+
+def test_multi_scheme_attention_errors():
+    L = S.lib()
+    g1, g2 = _g(), _g(bt=1, bh=8, bw=2)
+    geoms = (S.spade_geom * 2)(g1, g2)
+    heads = (S.spade_head_lists * 2)(S.spade_head_lists(0, 0x1000, 0x1000, 0, 0),
+                                     S.spade_head_lists(1, 0x1000, 0x1000, 0, 0))
+    call = lambda gs, n, hs, scale=0.1: L.spade_sparse_attn_raster_multi(  # noqa: E731
+        gs, n, hs, FAKE, FAKE, FAKE, scale, FAKE, NULL, NULL, 0, None)
+    assert call(geoms, 0, heads) == S.SPADE_ERR_INVALID_ARG                  # no geometry
+    assert call(geoms, 9, heads) == S.SPADE_ERR_INVALID_ARG                  # more than 8
+    assert call(geoms, 2, heads, scale=0.0) == S.SPADE_ERR_INVALID_ARG
+    other = (S.spade_geom * 2)(g1, _g(T=6))                                  # different grid
+    assert call(other, 2, heads) == S.SPADE_ERR_INVALID_ARG
+    bad = (S.spade_head_lists * 2)(S.spade_head_lists(0, 0x1000, 0x1000, 0, 0),
+                                   S.spade_head_lists(2, 0x1000, 0x1000, 0, 0))
+    assert call(geoms, 2, bad) == S.SPADE_ERR_INVALID_ARG                    # scheme 2 of 2
+    nul = (S.spade_head_lists * 2)(S.spade_head_lists(0, 0x1000, 0x1000, 0, 0),
+                                   S.spade_head_lists(1, 0, 0x1000, 0, 0))
+    assert call(geoms, 2, nul) == S.SPADE_ERR_INVALID_ARG                    # null counts
+    assert call(geoms, 2, None) == S.SPADE_ERR_INVALID_ARG
+    many = (S.spade_geom * 1)(_g(H=65))
+    assert call(many, 1, heads) == S.SPADE_ERR_UNSUPPORTED                   # H > 64
+    empty = (S.spade_geom * 1)(_g(B=0))
+    assert call(empty, 1, None) == S.SPADE_OK

@@ -128,9 +128,9 @@ def _check_choice(as_gpu, as_ref, choice_gpu):
     return ch_ref
 
 
-def _sweep_path(cfg, cands, sparsity):
+def _sweep_path(cfg, cands, sparsity, raster=False):
     return SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cands,
-                     sparsity, device=DEV)
+                     sparsity, device=DEV, raster=raster)
 
 
 @pytest.mark.parametrize("d", [64, 128])
@@ -237,3 +237,23 @@ def test_sweep_full_hunyuan_shape():
             assert np.array_equal(out[:, grp[jj]], got[:, j][:, pos])
     _say(f"  attention max-abs over sampled query blocks: {worst:.3e}")
     assert worst <= P.ATTN_MAX_ABS
+
+
+@pytest.mark.parametrize("case", ["small_d64", "small_d128_b2", "hunyuan"])
+def test_sweep_raster_multi_equals_grouped(case):
+    """One multi-scheme raster call gives every head exactly the output of its
+    group's blocked path (same rows, same arithmetic, same order)."""
+    if case == "hunyuan":
+        cfg, cands, sp = workload("hunyuan_sweep"), SWEEP_CANDIDATES, 0.85
+    elif case == "small_d64":
+        cfg = P.small_cfg(6, 16, 20, 1, 1, 1, d=64, H=6)
+        cands, sp = [(2, 4, 4), (3, 4, 5), (2, 8, 2), (1, 16, 4)], 0.6
+    else:
+        cfg = P.small_cfg(5, 11, 13, 1, 1, 1, d=128, H=5, B=2)
+        cands, sp = [(2, 4, 4), (3, 4, 5), (5, 3, 3)], 0.7
+    _say("raster multi sweep", case)
+    Q, K, V = P.bf16_inputs(cfg)
+    a = _sweep_path(cfg, cands, sp).run(Q, K, V)
+    b = _sweep_path(cfg, cands, sp, raster=True).run(Q, K, V)
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
