@@ -38,7 +38,8 @@ namespace {
 constexpr int kRows = 16;
 constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kMaxS = kMaxSelectNB / 64;  // register slots per lane
+// Register slots per lane of a row's keys (element e = 64 s + lane): SM slots
+// hold rows of up to 64 SM blocks; launches pick the smallest of 4, 8, 16.
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ void wave_sync() {
@@ -98,7 +99,8 @@ struct Cut {
 // Radix search of one wave's keys (0 = no element) with weights w for the
 // largest t with W(key >= t) >= need. count_rule: the tie group fills the count
 // (Top-K); otherwise the mass (Top-P). hw/hc: this wave's LDS histograms.
-__device__ Cut find_cut(const uint64_t (&key)[kMaxS], const uint64_t (&w)[kMaxS], uint64_t need,
+template <int SM>
+__device__ Cut find_cut(const uint64_t (&key)[SM], const uint64_t (&w)[SM], uint64_t need,
                         bool count_rule, uint64_t* hw, unsigned* hc, int lane) {
   uint64_t prefix = 0, above = 0, tstar = 0;
   for (int pass = 0; pass < 8; ++pass) {
@@ -110,7 +112,7 @@ __device__ Cut find_cut(const uint64_t (&key)[kMaxS], const uint64_t (&w)[kMaxS]
     }
     wave_sync();
 #pragma unroll
-    for (int s = 0; s < kMaxS; ++s) {
+    for (int s = 0; s < SM; ++s) {
       const bool cand =
           key[s] != 0 && (pass == 0 || (key[s] >> (shift + 8)) == (prefix >> (shift + 8)));
       if (cand) {
@@ -157,7 +159,7 @@ __device__ Cut find_cut(const uint64_t (&key)[kMaxS], const uint64_t (&w)[kMaxS]
     if (cD == 1) {  // a single element in the bucket: its key is the cut
       uint64_t kk = 0;
 #pragma unroll
-      for (int s = 0; s < kMaxS; ++s)
+      for (int s = 0; s < SM; ++s)
         if (key[s] != 0 && (key[s] >> shift) == (prefix >> shift)) kk = key[s];
       tstar = wave_max_u64(kk);
       break;
@@ -172,7 +174,7 @@ __device__ Cut find_cut(const uint64_t (&key)[kMaxS], const uint64_t (&w)[kMaxS]
   int n_above = 0, n_tie = 0;
   uint64_t w_above = 0, w_tie = 0;
 #pragma unroll
-  for (int s = 0; s < kMaxS; ++s) {
+  for (int s = 0; s < SM; ++s) {
     const bool gt = key[s] > tstar, eq = key[s] == tstar;
     n_above += __popcll(__ballot(gt));
     n_tie += __popcll(__ballot(eq));
@@ -213,20 +215,21 @@ __device__ __forceinline__ double coherence(const DevGeom& g, const double* sics
 // Marks of the intra Top-K filter over one head's blocks: the `k` least
 // coherent (ties to the lower index), written as 1s into mark[e - lo] for
 // lo <= e < hi. One wave.
+template <int SM>
 __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, int lo, int hi,
                                  unsigned char* mark, uint64_t* hw, unsigned* hc, int lane) {
   const int NB = g.NB;
-  uint64_t key[kMaxS], w[kMaxS];
+  uint64_t key[SM], w[SM];
 #pragma unroll
-  for (int s = 0; s < kMaxS; ++s) {
+  for (int s = 0; s < SM; ++s) {
     const int e = s * 64 + lane;
     key[s] = e < NB ? order_key(-coherence(g, sics, e) + 0.0) : 0;  // least coherent first
     w[s] = key[s] != 0 ? 1 : 0;
   }
-  const Cut c = find_cut(key, w, uint64_t(min(k, NB)), true, hw, hc, lane);
+  const Cut c = find_cut<SM>(key, w, uint64_t(min(k, NB)), true, hw, hc, lane);
   int tie_base = 0;
 #pragma unroll
-  for (int s = 0; s < kMaxS; ++s) {
+  for (int s = 0; s < SM; ++s) {
     const int e = s * 64 + lane;
     const bool eq = key[s] != 0 && key[s] == c.tstar;
     const uint64_t be = __ballot(eq);
@@ -237,8 +240,12 @@ __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, in
   }
 }
 
-template <int D, int EST>
-__global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec p) {
+// Rows of up to 512 blocks (SM <= 8) fit in 128 VGPRs outside the DSA estimator:
+// four waves per SIMD, two workgroups per CU.
+template <int D, int EST, int SM>
+__global__ void __launch_bounds__(kThreads)
+    __attribute__((amdgpu_waves_per_eu(SM <= 8 && EST != kEstDsa ? 4 : 1)))
+    select_kernel(DevGeom g, SelectSpec p) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int NB = g.NB;
   double* sc = reinterpret_cast<double*>(smem);                           // [kRows][NB]
@@ -287,13 +294,11 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
       const double2* pk = reinterpret_cast<const double2*>(k0 + co) + g4;
       f64x4 acc = {0.0, 0.0, 0.0, 0.0};
       if (EST == kEstMean) {
-        double2 kv[KQ];
-#pragma unroll
-        for (int kq = 0; kq < KQ; ++kq) kv[kq] = pk[4 * kq];
 #pragma unroll
         for (int kq = 0; kq < KQ; ++kq) {
-          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq], kv[kq].x, acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq + 1], kv[kq].y, acc, 0, 0, 0);
+          const double2 kv = pk[4 * kq];
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq], kv.x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(qa[2 * kq + 1], kv.y, acc, 0, 0, 0);
         }
       } else {
         const double2* pn = reinterpret_cast<const double2*>(p.k1 + bh * NB * D + co) + g4;
@@ -377,10 +382,11 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
   __syncthreads();
   if (p.intra == kIntraTopk && p.intra_k > 0) {
     if (wave == 0)
-      intra_topk_marks(g, p.sics_k + bh * NB, p.intra_k, 0, NB, colmark, hist_w, hist_c, lane);
+      intra_topk_marks<SM>(g, p.sics_k + bh * NB, p.intra_k, 0, NB, colmark, hist_w, hist_c,
+                           lane);
     else if (wave == 1)
-      intra_topk_marks(g, p.sics_q + bh * NB, p.intra_k, i0, i0 + kRows, rowmark, hist_w + 256,
-                       hist_c + 256, lane);
+      intra_topk_marks<SM>(g, p.sics_q + bh * NB, p.intra_k, i0, i0 + kRows, rowmark,
+                           hist_w + 256, hist_c + 256, lane);
     __syncthreads();
   }
 
@@ -402,10 +408,10 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
       continue;
     }
 
-    uint64_t key[kMaxS], w[kMaxS];
+    uint64_t key[SM], w[SM];
     double smax = -INFINITY;
 #pragma unroll
-    for (int s = 0; s < kMaxS; ++s) {
+    for (int s = 0; s < SM; ++s) {
       key[s] = 0;
       w[s] = 0;
       const int e = s * 64 + lane;
@@ -418,13 +424,13 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
     uint64_t need;
     if (p.mode == 0) {
 #pragma unroll
-      for (int s = 0; s < kMaxS; ++s) w[s] = key[s] != 0 ? 1 : 0;
+      for (int s = 0; s < SM; ++s) w[s] = key[s] != 0 ? 1 : 0;
       need = uint64_t(min(topk, NB));
     } else {
       smax = wave_max_f64(smax);
       uint64_t z = 0;
 #pragma unroll
-      for (int s = 0; s < kMaxS; ++s) {
+      for (int s = 0; s < SM; ++s) {
         const int e = s * 64 + lane;
         if (key[s] != 0) {
           const double ev = exp(sc[rr * NB + e] - smax);       // in (0, 1]
@@ -437,7 +443,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
       need = uint64_t(ceil(t * double(z)));
       need = need < 1 ? 1 : (need > z ? z : need);
     }
-    const Cut c = find_cut(key, w, need, p.mode == 0, hw, hc, lane);
+    const Cut c = find_cut<SM>(key, w, need, p.mode == 0, hw, hc, lane);
 
     int cnt_out = 0;
     if (c.all) {
@@ -447,7 +453,7 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
       const int ci = window ? coord[row] : 0;
       int tie_base = 0;
 #pragma unroll
-      for (int s = 0; s < kMaxS; ++s) {
+      for (int s = 0; s < SM; ++s) {
         const int e = s * 64 + lane;
         const bool eq = key[s] == c.tstar;
         const uint64_t be = __ballot(eq);
@@ -465,22 +471,29 @@ __global__ void __launch_bounds__(kThreads) select_kernel(DevGeom g, SelectSpec 
   }
 }
 
-template <int D, int EST>
-hipError_t launch_de(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
+template <int D, int EST, int SM>
+hipError_t launch_des(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
   const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * (8 + 4) +
                      size_t(g.NB) * (4 + 1) + kRows;
   static bool attr_set = false;  // raising the dynamic-LDS cap once is idempotent
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&select_kernel<D, EST>),
+        reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
         hipFuncAttributeMaxDynamicSharedMemorySize,
         int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 12 + kMaxSelectNB * 5 + kRows));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
   const dim3 grid((g.NB + kRows - 1) / kRows, g.B * g.H);
-  select_kernel<D, EST><<<grid, kThreads, lds, s>>>(g, p);
+  select_kernel<D, EST, SM><<<grid, kThreads, lds, s>>>(g, p);
   return hipGetLastError();
+}
+
+template <int D, int EST>
+hipError_t launch_de(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
+  if (g.NB <= 256) return launch_des<D, EST, 4>(g, p, s);
+  if (g.NB <= 512) return launch_des<D, EST, 8>(g, p, s);
+  return launch_des<D, EST, 16>(g, p, s);
 }
 
 template <int D>
