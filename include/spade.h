@@ -302,8 +302,10 @@ spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_
                                   hipStream_t stream);
 
 /*
- * Scratch bytes spade_block_sparse_attn needs for its work schedule (the
- * ranked work list of §3.3's optimisation (3)); 0 for an empty problem.
+ * Scratch bytes spade_block_sparse_attn and spade_sparse_attn_raster need for
+ * their work schedule (§3.3 optimisation (3): the mask preprocessed into a ranked
+ * layout, heads of similar density co-scheduled): 12 bytes per (batch, head)
+ * pair, 0 for an empty problem or more than 4096 pairs (grid order then).
  */
 size_t spade_attn_workspace_bytes(const spade_geom* g);
 
@@ -322,8 +324,12 @@ size_t spade_attn_workspace_bytes(const spade_geom* g);
  *            padding slots are written 0. A row with no kept block gets 0.
  *   lse:     out, nullable, fp32 [B,H,NB*BS]: natural-log softmax denominator
  *            (max included) per real query slot; padding slots are not written.
- *   workspace: device scratch of at least spade_attn_workspace_bytes(g) bytes
- *            (contents on entry do not matter).
+ *   workspace: device scratch of at least spade_attn_workspace_bytes(g) bytes,
+ *            16-byte aligned (contents on entry do not matter). The call ranks the
+ *            (batch, head) pairs there by their heaviest row, then their total kept
+ *            blocks, and dispatches the heaviest first, so long rows do not form
+ *            the launch's tail; results do not depend on the order. A workspace
+ *            serves one call at a time (calls that share one must be ordered).
  *   bf16 MFMA with fp32 accumulation; softmax in fp32; P rounded to bf16 for
  *   the P*V product; output rounded to bf16 (round to nearest even).
  */

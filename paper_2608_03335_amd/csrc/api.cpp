@@ -110,9 +110,9 @@ spade_status sparse_attn(const spade_geom* g, const void* q, const void* k, cons
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
     return fail(SPADE_ERR_INVALID_ARG, "q, k, v and o must be 16-byte aligned");
   const size_t need = spade::attn_workspace_bytes(dg);
-  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
-    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
-                workspace_bytes);
+  if (workspace_bytes < need || (need > 0 && (workspace == nullptr || !aligned16(workspace))))
+    return fail(SPADE_ERR_WORKSPACE, "16-byte aligned workspace of %zu bytes needed, %zu given",
+                need, workspace_bytes);
   return hip_status(spade::launch_block_sparse_attn(dg, q, k, v, counts, indices, float(scale), o,
                                                     lse, workspace, raster, stream),
                     "sparse attention launch");

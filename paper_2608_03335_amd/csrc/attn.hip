@@ -237,7 +237,7 @@ __global__ void __launch_bounds__(64 * (W + LD))
     attn_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
                 const char* __restrict__ vb, const int* __restrict__ counts,
                 const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
-                float* __restrict__ lse,
+                float* __restrict__ lse, const int* __restrict__ order,
                 typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
   using TL = Tile<D>;
   __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
@@ -276,6 +276,7 @@ __global__ void __launch_bounds__(64 * (W + LD))
     const int per_xcd = (g.NB + 7) / 8;
     const int64_t slot = int64_t(blockIdx.x) >> 3;
     bh = slot / per_xcd;
+    if (order) bh = order[bh];  // heads in the ranked order (heaviest first)
     i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
     if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
     cnt_src = counts + bh * g.NB + i;
@@ -503,7 +504,7 @@ __global__ void __launch_bounds__(64 * (W + LD))
 template <int D, int W, bool LD, bool RASTER, bool MULTI>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
-                     hipStream_t s, const MultiTable* tab = nullptr) {
+                     hipStream_t s, const MultiTable* tab = nullptr, const int* order = nullptr) {
   static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(
@@ -522,12 +523,12 @@ hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const voi
     const int64_t items = int64_t(g.B) * tab->items_per_batch;
     attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
                                            size_t(nb_max) * sizeof(int), s>>>(
-        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, *tab);
+        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, nullptr, *tab);
   } else {
     const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
     attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
                                            size_t(g.NB) * sizeof(int), s>>>(
-        g, q4, k1, v1, counts, indices, scale_log2, o2, lse, NoTable{});
+        g, q4, k1, v1, counts, indices, scale_log2, o2, lse, order, NoTable{});
   }
   return hipGetLastError();
 }
@@ -535,11 +536,11 @@ hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const voi
 template <int D, bool RASTER, bool MULTI = false>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
-                    hipStream_t s, const MultiTable* tab = nullptr) {
+                    hipStream_t s, const MultiTable* tab = nullptr, const int* order = nullptr) {
 #define SPADE_ATTN_CASE(w, ld)                                                                  \
   case w:                                                                                       \
     return launch_dw<D, w, ld, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob, \
-                                              lse, s, tab);
+                                              lse, s, tab, order);
   // loader wave unless it would cost a workgroup per CU (4 or 6 compute waves)
   switch ((g.BS + 31) / 32) {
     SPADE_ATTN_CASE(1, true) SPADE_ATTN_CASE(2, true) SPADE_ATTN_CASE(3, true)
@@ -550,9 +551,63 @@ hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void
   return hipErrorInvalidValue;
 }
 
+// Ranked work order (§3.3 (3): rows preprocessed into a ranked layout, heads of
+// similar density co-scheduled). The dispatch walks the (batch, head) pairs in
+// the order of their heaviest row, then their total kept blocks (descending,
+// ties to the lower index), so long rows start first instead of forming the
+// tail; within a head the XCD mapping is unchanged.
+constexpr int kRankThreads = 1024;
+constexpr int kMaxRankedHeads = 4096;  // beyond this many (batch, head) pairs: grid order
+
+__global__ void __launch_bounds__(256) head_keys_kernel(DevGeom g, const int* __restrict__ counts,
+                                                        uint64_t* __restrict__ keys) {
+  __shared__ int smax[256];
+  __shared__ uint32_t ssum[256];
+  const int64_t bh = blockIdx.x;
+  int mx = 0;
+  uint32_t sum = 0;
+  for (int i = threadIdx.x; i < g.NB; i += 256) {
+    const int c = min(max(counts[bh * g.NB + i], 0), g.NB);
+    mx = max(mx, c);
+    sum += uint32_t(c);
+  }
+  smax[threadIdx.x] = mx;
+  ssum[threadIdx.x] = sum;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (threadIdx.x < st) {
+      smax[threadIdx.x] = max(smax[threadIdx.x], smax[threadIdx.x + st]);
+      ssum[threadIdx.x] += ssum[threadIdx.x + st];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) keys[bh] = (uint64_t(uint32_t(smax[0])) << 32) | ssum[0];
+}
+
+__global__ void __launch_bounds__(kRankThreads) head_rank_kernel(const uint64_t* __restrict__ keys,
+                                                                 int n, int* __restrict__ order) {
+  for (int t = threadIdx.x; t < n; t += kRankThreads) {
+    const uint64_t kt = keys[t];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      const uint64_t kj = keys[j];
+      rank += (kj > kt || (kj == kt && j < t)) ? 1 : 0;
+    }
+    order[rank] = t;
+  }
+}
+
+size_t ranked_pairs(const DevGeom& g) {
+  const int64_t n = int64_t(g.B) * g.H;
+  return n > 0 && n <= kMaxRankedHeads ? size_t(n) : 0;
+}
+
 }  // namespace
 
-size_t attn_workspace_bytes(const DevGeom&) { return 0; }
+size_t attn_workspace_bytes(const DevGeom& g) {
+  const size_t n = ranked_pairs(g);  // keys (8 B) then the order (4 B) of every pair
+  return n ? n * 8 + n * 4 : 0;
+}
 
 hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHead* heads,
                                     int n_heads, const void* q, const void* k, const void* v,
@@ -585,15 +640,25 @@ hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHe
 
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,
-                                    float scale, void* ob, float* lse, void*, bool raster,
+                                    float scale, void* ob, float* lse, void* ws, bool raster,
                                     hipStream_t s) {
   const float sl2 = scale * 1.44269504088896340736f;
+  const int* order = nullptr;
+  if (const size_t n = ranked_pairs(g)) {
+    uint64_t* keys = static_cast<uint64_t*>(ws);
+    int* ord = reinterpret_cast<int*>(keys + n);
+    head_keys_kernel<<<dim3(unsigned(n)), 256, 0, s>>>(g, counts, keys);
+    head_rank_kernel<<<1, kRankThreads, 0, s>>>(keys, int(n), ord);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    order = ord;
+  }
   if (g.d == 128)
-    return raster ? launch_d<128, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s)
-                  : launch_d<128, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s);
+    return raster ? launch_d<128, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s, nullptr, order)
+                  : launch_d<128, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s, nullptr, order);
   if (g.d == 64)
-    return raster ? launch_d<64, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s)
-                  : launch_d<64, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s);
+    return raster ? launch_d<64, true>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s, nullptr, order)
+                  : launch_d<64, false>(g, qb, kb, vb, counts, indices, sl2, ob, lse, s, nullptr, order);
   return hipErrorInvalidValue;
 }
 

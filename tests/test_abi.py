@@ -210,6 +210,14 @@ def test_attention_workspace_and_pointer_errors():
     st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, -1.0, FAKE,
                                    NULL, FAKE, need, None)
     assert st == S.SPADE_ERR_INVALID_ARG
+    # the ranked work order: 8 + 4 bytes per (batch, head) pair
+    assert need == g.B * g.H * 12
+    st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE,
+                                   NULL, NULL, need, None)
+    assert st == S.SPADE_ERR_WORKSPACE
+    st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE,
+                                   NULL, MISALIGNED, need, None)
+    assert st == S.SPADE_ERR_WORKSPACE
 
 
 def test_python_binding_raises_with_message():

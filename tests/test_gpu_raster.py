@@ -40,7 +40,8 @@ def test_raster_equals_blocked_then_restore(name):
     p.restore()
     o = torch.full_like(Q, float("nan"))
     lse = torch.full((cfg["B"], cfg["H"], g.N), float("nan"), dtype=torch.float32, device=DEV)
-    S.spade_sparse_attn_raster(g, Q, K, V, counts, indices, P.scale_of(cfg["d"]), o, lse)
+    S.spade_sparse_attn_raster(g, Q, K, V, counts, indices, P.scale_of(cfg["d"]), o, lse,
+                               workspace=p.ws)
     torch.cuda.synchronize()
     assert torch.equal(o.view(torch.int16), p.O.view(torch.int16))
     pos = torch.from_numpy(O.token_position(P.geometry(cfg))).to(DEV)
