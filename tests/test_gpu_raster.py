@@ -78,3 +78,40 @@ def test_raster_full_hunyuan_equals_blocked():
     torch.cuda.synchronize()
     assert torch.equal(p.counts, pv.counts)
     assert torch.equal(p.O.view(torch.int16), pv.O.view(torch.int16))
+
+
+@pytest.mark.parametrize("name,n_rows", [("wan13b", 16), ("hunyuan", 16), ("wan14b", 12)])
+def test_full_shape_raster_path(name, n_rows):
+    """The path bench.py times (raster form) at the full layer shapes: every row's
+    selection against the oracle, and sampled query blocks (first and last included)
+    recomputed by the oracle with the GPU's lists, O and LSE."""
+    from gen.workloads import workload
+    cfg = workload(name)
+    _say("raster full shape", name)
+    og = P.geometry(cfg)
+    Q, K, V = P.bf16_inputs(cfg)
+    p = _path(cfg, virtual=True, with_lse=True)
+    p.run(Q, K, V)
+    torch.cuda.synchronize()
+    s, c, i = _oracle_selection(cfg, Q, K, cfg["mode"], cfg.get("topk"), cfg.get("tau"))
+    n_ex = P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(),
+                               cfg["mode"], cfg.get("tau"))
+    _say(f"  selection rows exempt: {n_ex}")
+    cg, ig = p.counts.cpu().numpy(), p.indices.cpu().numpy()
+    rows = P.sample_rows(cfg["B"], cfg["H"], og.NB, n_rows, seed=2,
+                         must=[(0, 0, 0), (0, cfg["H"] - 1, og.NB - 1)])
+    heads = sorted({h for _, h, _ in rows})
+    sub = [(b, heads.index(h), i) for b, h, i in rows]
+    Qb, Kb, Vb = (O.reorder(P.to_np64(x[:, heads]), og) for x in (Q, K, V))
+    ref, ref_lse = O.block_sparse_attention(Qb, Kb, Vb, cg[:, heads], ig[:, heads], og,
+                                            P.scale_of(cfg["d"]), rows=sub)
+    slot_token, nv = O.block_tables(og)
+    got, got_lse = P.to_np64(p.O[:, heads]), p.lse[:, heads].cpu().numpy()
+    worst = 0.0
+    for (b, k, i) in sub:
+        toks = slot_token[i * og.BS: i * og.BS + nv[i]]
+        sl = slice(i * og.BS, i * og.BS + nv[i])
+        worst = max(worst, float(np.max(np.abs(got[b, k, toks] - ref[b, k, sl]))))
+        np.testing.assert_allclose(got_lse[b, k, toks], ref_lse[b, k, sl], atol=P.LSE_MAX_ABS, rtol=0)
+    _say(f"  attention max-abs over {len(sub)} sampled query blocks: {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
