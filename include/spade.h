@@ -304,8 +304,9 @@ spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_
 /*
  * Scratch bytes spade_block_sparse_attn and spade_sparse_attn_raster need for
  * their work schedule (§3.3 optimisation (3): the mask preprocessed into a ranked
- * layout, heads of similar density co-scheduled): 12 bytes per (batch, head)
- * pair, 0 for an empty problem or more than 4096 pairs (grid order then).
+ * layout, heads of similar density co-scheduled), and spade_sparse_attn_raster_multi
+ * for the same: 16 bytes per (batch, head) pair, 0 for an empty problem or more
+ * than 4096 pairs (grid order then).
  */
 size_t spade_attn_workspace_bytes(const spade_geom* g);
 
@@ -378,7 +379,10 @@ typedef struct {
  *            H, d and the grid (T, Hs, Ws). H <= 64.
  *   heads:   HOST array [H]: per head its blocking and block lists (any layout, e.g.
  *            per-group buffers written by spade_compose_select with a head list).
- *   q, k, v, scale, o, lse, workspace: as for spade_sparse_attn_raster.
+ *   q, k, v, scale, o, lse: as for spade_sparse_attn_raster.
+ *   workspace: spade_attn_workspace_bytes(&geoms[0]) bytes, 16-byte aligned
+ *            (contents on entry do not matter); each launch ranks its heads there
+ *            per batch element, heaviest first, as spade_block_sparse_attn does.
  *   Each head's output equals spade_sparse_attn_raster's under its own blocking,
  *   bit for bit. Heads whose blocks need the same number of 32-row waves
  *   (ceil(BS/32)) run in one launch: one launch in total when all blockings

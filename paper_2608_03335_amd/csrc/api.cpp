@@ -344,11 +344,11 @@ spade_status spade_sparse_attn_raster_multi(const spade_geom* geoms, int32_t n_g
     mh[h] = {x.counts, x.indices, x.indices_bstride, int(x.counts_bstride), x.scheme, h, 0};
   }
   const size_t need = spade::attn_workspace_bytes(dg[0]);
-  if (workspace_bytes < need || (need > 0 && workspace == nullptr))
-    return fail(SPADE_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
-                workspace_bytes);
+  if (workspace_bytes < need || (need > 0 && (workspace == nullptr || !aligned16(workspace))))
+    return fail(SPADE_ERR_WORKSPACE, "16-byte aligned workspace of %zu bytes needed, %zu given",
+                need, workspace_bytes);
   return hip_status(spade::launch_sparse_attn_multi(dg, n_geoms, mh, dg[0].H, q, k, v,
-                                                    float(scale), o, lse, stream),
+                                                    float(scale), o, lse, workspace, stream),
                     "multi-scheme attention launch");
 }
 

@@ -30,6 +30,7 @@
 // raised (and O rescaled) when some row's max grows by more than 2^8, so most
 // chunks skip the 64-register rescale; row sums use bf16 dot2 on the same packed
 // P that feeds the MFMA.
+#include <climits>
 #include <type_traits>
 
 #include "spade_internal.h"
@@ -261,11 +262,25 @@ __global__ void __launch_bounds__(64 * (W + LD))
   if constexpr (MULTI) {
     const int b = int(blockIdx.x) / tab.items_per_batch;
     const int w = int(blockIdx.x) - b * tab.items_per_batch;
-    int k = 0;
-    while (k + 1 < tab.n_heads && tab.head[k + 1].start <= w) ++k;
+    int k = 0, start;
+    if (order) {
+      // ranked: order holds per batch element the launch's heads by rank, then
+      // their ascending first items; the item's rank is the number of first
+      // items <= w, minus one (one load per lane and a ballot, n_heads <= 64)
+      const int n = tab.n_heads;
+      const int* ranked = order + int64_t(b) * 2 * n;
+      const int ln = int(threadIdx.x & 63);
+      const int first = ln < n ? ranked[n + ln] : INT_MAX;
+      const int r = __popcll(__ballot(first <= w)) - 1;
+      k = __builtin_amdgcn_readfirstlane(ranked[r]);
+      start = __builtin_amdgcn_readfirstlane(ranked[n + r]);
+    } else {
+      while (k + 1 < tab.n_heads && tab.head[k + 1].start <= w) ++k;
+      start = tab.head[k].start;
+    }
     const MultiHead& mh = tab.head[k];
     g = tab.geo[mh.geom];
-    const int local = w - mh.start;  // same residue mod 8 as blockIdx.x
+    const int local = w - start;  // same residue mod 8 as blockIdx.x
     const int per_xcd = (g.NB + 7) / 8;
     i = (local & 7) * per_xcd + (local >> 3);
     if (i >= g.NB) return;
@@ -523,7 +538,7 @@ hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const voi
     const int64_t items = int64_t(g.B) * tab->items_per_batch;
     attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
                                            size_t(nb_max) * sizeof(int), s>>>(
-        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, nullptr, *tab);
+        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, order, *tab);
   } else {
     const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
     attn_kernel<D, W, LD, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (W + LD),
@@ -597,6 +612,68 @@ __global__ void __launch_bounds__(kRankThreads) head_rank_kernel(const uint64_t*
   }
 }
 
+// The same ranking for one multi-scheme launch, per batch element over the
+// launch's heads; the heads' first items follow as prefix sums of their padded
+// item counts in rank order. Layout of `ranked`: per batch element, n head
+// indices by rank, then n first items.
+__global__ void __launch_bounds__(256) multi_keys_kernel(MultiTable tab,
+                                                         uint64_t* __restrict__ keys) {
+  __shared__ int smax[256];
+  __shared__ uint32_t ssum[256];
+  const int n = tab.n_heads;
+  const int b = int(blockIdx.x) / n, k = int(blockIdx.x) - b * n;
+  const MultiHead& mh = tab.head[k];
+  const int NB = tab.geo[mh.geom].NB;
+  const int* cnt = mh.counts + int64_t(b) * mh.counts_bstride;
+  int mx = 0;
+  uint32_t sum = 0;
+  for (int i = threadIdx.x; i < NB; i += 256) {
+    const int c = min(max(cnt[i], 0), NB);
+    mx = max(mx, c);
+    sum += uint32_t(c);
+  }
+  smax[threadIdx.x] = mx;
+  ssum[threadIdx.x] = sum;
+  __syncthreads();
+  for (int st = 128; st > 0; st >>= 1) {
+    if (threadIdx.x < st) {
+      smax[threadIdx.x] = max(smax[threadIdx.x], smax[threadIdx.x + st]);
+      ssum[threadIdx.x] += ssum[threadIdx.x + st];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) keys[blockIdx.x] = (uint64_t(uint32_t(smax[0])) << 32) | ssum[0];
+}
+
+__global__ void __launch_bounds__(64) multi_rank_kernel(MultiTable tab,
+                                                        const uint64_t* __restrict__ keys,
+                                                        int* __restrict__ ranked) {
+  __shared__ int by_rank[kMaxMultiHeads];
+  const int n = tab.n_heads, b = blockIdx.x;
+  const uint64_t* kb = keys + int64_t(b) * n;
+  const int t = threadIdx.x;
+  if (t < n) {
+    const uint64_t kt = kb[t];
+    int rank = 0;
+    for (int j = 0; j < n; ++j) {
+      const uint64_t kj = kb[j];
+      rank += (kj > kt || (kj == kt && j < t)) ? 1 : 0;
+    }
+    by_rank[rank] = t;
+  }
+  __syncthreads();
+  if (t == 0) {
+    int* out = ranked + int64_t(b) * 2 * n;
+    int first = 0;
+    for (int r = 0; r < n; ++r) {
+      const int k = by_rank[r];
+      out[r] = k;
+      out[n + r] = first;
+      first += (tab.geo[tab.head[k].geom].NB + 7) / 8 * 8;
+    }
+  }
+}
+
 size_t ranked_pairs(const DevGeom& g) {
   const int64_t n = int64_t(g.B) * g.H;
   return n > 0 && n <= kMaxRankedHeads ? size_t(n) : 0;
@@ -605,14 +682,19 @@ size_t ranked_pairs(const DevGeom& g) {
 }  // namespace
 
 size_t attn_workspace_bytes(const DevGeom& g) {
-  const size_t n = ranked_pairs(g);  // keys (8 B) then the order (4 B) of every pair
-  return n ? n * 8 + n * 4 : 0;
+  // keys (8 B) of every pair, then the order (4 B; a multi-scheme launch also
+  // keeps each head's first item, 4 B more)
+  const size_t n = ranked_pairs(g);
+  return n ? n * 16 : 0;
 }
 
 hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHead* heads,
                                     int n_heads, const void* q, const void* k, const void* v,
-                                    float scale, void* o, float* lse, hipStream_t s) {
+                                    float scale, void* o, float* lse, void* ws, hipStream_t s) {
   const float sl2 = scale * 1.44269504088896340736f;
+  // each launch ranks its heads in its own part of the workspace (16 B per pair)
+  const bool rank = ranked_pairs(geo[0]) > 0;
+  char* wsp = static_cast<char*>(ws);
   // one launch per workgroup shape; the launch's geometry carries that shape's BS
   for (int w = 1; w <= kMaxBS / 32; ++w) {
     MultiTable tab = {};
@@ -630,9 +712,21 @@ hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHe
     if (tab.n_heads == 0) continue;
     tab.items_per_batch = start;
     const DevGeom& gl = geo[widest];
+    const int* order = nullptr;
+    if (rank) {
+      const int64_t pairs = int64_t(gl.B) * tab.n_heads;
+      uint64_t* keys = reinterpret_cast<uint64_t*>(wsp);
+      int* ranked = reinterpret_cast<int*>(keys + pairs);
+      wsp += pairs * 16;
+      multi_keys_kernel<<<dim3(unsigned(pairs)), 256, 0, s>>>(tab, keys);
+      multi_rank_kernel<<<dim3(unsigned(gl.B)), 64, 0, s>>>(tab, keys, ranked);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      order = ranked;
+    }
     const hipError_t e = gl.d == 128
-        ? launch_d<128, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab)
-        : launch_d<64, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab);
+        ? launch_d<128, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab, order)
+        : launch_d<64, true, true>(gl, q, k, v, nullptr, nullptr, sl2, o, lse, s, &tab, order);
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

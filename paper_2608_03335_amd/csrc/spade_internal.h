@@ -137,7 +137,7 @@ struct MultiTable {
 // whose blockings share a shape run in the same launch.
 hipError_t launch_sparse_attn_multi(const DevGeom* geo, int n_geo, const MultiHead* heads,
                                     int n_heads, const void* q, const void* k, const void* v,
-                                    float scale, void* o, float* lse, hipStream_t s);
+                                    float scale, void* o, float* lse, void* ws, hipStream_t s);
 hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void* kb,
                                     const void* vb, const int* counts, const int* indices,
                                     float scale, void* ob, float* lse, void* ws, bool raster,

@@ -210,8 +210,9 @@ def test_attention_workspace_and_pointer_errors():
     st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, -1.0, FAKE,
                                    NULL, FAKE, need, None)
     assert st == S.SPADE_ERR_INVALID_ARG
-    # the ranked work order: 8 + 4 bytes per (batch, head) pair
-    assert need == g.B * g.H * 12
+    # the ranked work order: 16 bytes per (batch, head) pair (keys, order, and the
+    # first items a multi-scheme launch keeps)
+    assert need == g.B * g.H * 16
     st = L.spade_block_sparse_attn(ctypes.byref(g), FAKE, FAKE, FAKE, FAKE, FAKE, 0.125, FAKE,
                                    NULL, NULL, need, None)
     assert st == S.SPADE_ERR_WORKSPACE
@@ -335,3 +336,11 @@ def test_multi_scheme_attention_errors():
     assert call(many, 1, heads) == S.SPADE_ERR_UNSUPPORTED                   # H > 64
     empty = (S.spade_geom * 1)(_g(B=0))
     assert call(empty, 1, None) == S.SPADE_OK
+    # the workspace of the per-launch head ranking
+    need = L.spade_attn_workspace_bytes(ctypes.byref(g1))
+    assert need == g1.B * g1.H * 16
+    ws_call = lambda ws, n: L.spade_sparse_attn_raster_multi(  # noqa: E731
+        geoms, 2, heads, FAKE, FAKE, FAKE, 0.1, FAKE, NULL, ws, n, None)
+    assert ws_call(NULL, need) == S.SPADE_ERR_WORKSPACE
+    assert ws_call(FAKE, need - 1) == S.SPADE_ERR_WORKSPACE
+    assert ws_call(MISALIGNED, need) == S.SPADE_ERR_WORKSPACE
