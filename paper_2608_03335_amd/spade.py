@@ -4,6 +4,12 @@ Tensors are torch tensors used as device buffers; every step of the path runs in
 the library's HIP kernels. Each function raises SpadeError when the library
 returns a non-OK status. Calls are asynchronous on the given HIP stream
 (default: torch's current stream).
+
+The C ABI sees plain pointers and cannot tell a host buffer, a strided view, the
+wrong element type or a short buffer from a good one, so the binding checks each
+tensor before passing its pointer: on the GPU, contiguous, of the element type
+the header declares and at least as large as the geometry implies (raising
+SpadeError with SPADE_ERR_INVALID_ARG otherwise).
 """
 from __future__ import annotations
 
@@ -117,8 +123,66 @@ def lib() -> ctypes.CDLL:
     return _lib
 
 
-def _p(t):
-    return None if t is None else ctypes.c_void_p(t.data_ptr())
+BF16, F32, F64, I32 = torch.bfloat16, torch.float32, torch.float64, torch.int32
+
+
+class _Args:
+    """Checked device pointers of one call's tensors. Element type, layout and size
+    are checked as each tensor is added (None passes as NULL; dtype None: any;
+    numel None: unchecked), the device of all of them just before the call, so an
+    argument mistake is reported before a placement one."""
+
+    def __init__(self):
+        self.host = None
+
+    def __call__(self, t, dtype, numel, name):
+        if t is None:
+            return None
+        if not isinstance(t, torch.Tensor):
+            raise SpadeError(SPADE_ERR_INVALID_ARG, f"{name} must be a torch tensor")
+        if dtype is not None and t.dtype != dtype:
+            raise SpadeError(SPADE_ERR_INVALID_ARG, f"{name} must be {dtype} (got {t.dtype})")
+        if not t.is_contiguous():
+            raise SpadeError(SPADE_ERR_INVALID_ARG, f"{name} must be contiguous")
+        if numel is not None and t.numel() < numel:
+            raise SpadeError(SPADE_ERR_INVALID_ARG,
+                             f"{name} holds {t.numel()} elements, {numel} needed")
+        if not t.is_cuda and self.host is None:
+            self.host = name
+        return ctypes.c_void_p(t.data_ptr())
+
+    def ready(self):
+        if self.host is not None:
+            raise SpadeError(SPADE_ERR_INVALID_ARG, f"{self.host} must be a GPU tensor")
+
+    def run(self, fn, *args):
+        """Calls fn once every tensor has passed; the stream (the last argument, as
+        given by the caller) is resolved only then."""
+        self.ready()
+        return fn(*args[:-1], _s(args[-1]))
+
+
+class _Dims:
+    """Element counts of the tensors of one geometry (n: heads of the call), or
+    None everywhere when the geometry is invalid (the library then rejects it)."""
+
+    def __init__(self, g: spade_geom, n=None):
+        ok = min(g.bt, g.bh, g.bw) >= 1 and min(g.B, g.H, g.T, g.Hs, g.Ws) >= 0
+        nb = ((-(-g.T // g.bt)) * (-(-g.Hs // g.bh)) * (-(-g.Ws // g.bw))) if ok else 0
+        bh = g.B * (g.H if n is None else n)
+        full = g.B * g.H
+        N = g.T * g.Hs * g.Ws
+        BS = g.bt * g.bh * g.bw
+        v = (lambda x: x if ok else None)  # noqa: E731
+        self.raster = v(full * N * g.d)          # raster [B,H,N,d]
+        self.raster_rows = v(full * N)           # raster [B,H,N]
+        self.blocked = v(bh * nb * BS * g.d)     # blocked [B,n,NB*BS,d]
+        self.blocked_rows = v(bh * nb * BS)      # blocked [B,n,NB*BS]
+        self.summ = v(bh * nb * g.d)             # [B,n,NB,d]
+        self.per_block = v(bh * nb)              # [B,n,NB]
+        self.pairs = v(bh * nb * nb)             # [B,n,NB,NB]
+        self.per_head = v(bh)                    # [B,n]
+        self.NB = nb
 
 
 def _s(stream):
@@ -143,49 +207,80 @@ def _head_list(heads):
 
 def spade_block_reorder(g: spade_geom, x, y, inverse: bool = False, heads=None, stream=None):
     """heads: None (all heads) or a sequence of head indices (the group's heads)."""
-    dtype = SPADE_BF16 if x.dtype == torch.bfloat16 else SPADE_FP32
+    if not isinstance(x, torch.Tensor) or x.dtype not in (BF16, F32):
+        raise SpadeError(SPADE_ERR_INVALID_ARG, "x must be a bfloat16 or float32 tensor")
+    a = _Args()
     arr, n = _head_list(heads)
-    _check(lib().spade_block_reorder(ctypes.byref(g), _p(x), _p(y), dtype, int(inverse), arr, n,
-                                     _s(stream)))
+    D = _Dims(g, n if heads is not None else None)
+    src, dst = (D.blocked, D.raster) if inverse else (D.raster, D.blocked)
+    dtype = SPADE_BF16 if x.dtype == BF16 else SPADE_FP32
+    _check(a.run(lib().spade_block_reorder, ctypes.byref(g), a(x, x.dtype, src, "x"),
+                 a(y, x.dtype, dst, "y"), dtype, int(inverse), arr, n, stream))
 
 
 def spade_summarize(g: spade_geom, qb, kb, qbar, kbar, sics_q=None, sics_k=None, stream=None):
-    _check(lib().spade_summarize(ctypes.byref(g), _p(qb), _p(kb), _p(qbar), _p(kbar),
-                                 _p(sics_q), _p(sics_k), _s(stream)))
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_summarize, ctypes.byref(g), a(qb, BF16, D.blocked, "qb"),
+                 a(kb, BF16, D.blocked, "kb"), a(qbar, F64, D.summ, "qbar"),
+                 a(kbar, F64, D.summ, "kbar"), a(sics_q, F64, D.per_block, "sics_q"),
+                 a(sics_k, F64, D.per_block, "sics_k"), stream))
 
 
 def spade_block_summarize(g: spade_geom, q, k, qb=None, kb=None, qbar=None, kbar=None,
                           sics_q=None, sics_k=None, heads=None, stream=None):
+    a = _Args()
     arr, n = _head_list(heads)
-    _check(lib().spade_block_summarize(ctypes.byref(g), _p(q), _p(k), _p(qb), _p(kb), _p(qbar),
-                                       _p(kbar), _p(sics_q), _p(sics_k), arr, n, _s(stream)))
+    D = _Dims(g, n if heads is not None else None)
+    _check(a.run(lib().spade_block_summarize, ctypes.byref(g), a(q, BF16, D.raster, "q"),
+                 a(k, BF16, D.raster, "k"), a(qb, BF16, D.blocked, "qb"),
+                 a(kb, BF16, D.blocked, "kb"), a(qbar, F64, D.summ, "qbar"),
+                 a(kbar, F64, D.summ, "kbar"), a(sics_q, F64, D.per_block, "sics_q"),
+                 a(sics_k, F64, D.per_block, "sics_k"), arr, n, stream))
 
 
 def spade_aggregation_score(g: spade_geom, sics_q, sics_k, as_qk, as_q=None, as_k=None,
                             stream=None):
-    _check(lib().spade_aggregation_score(ctypes.byref(g), _p(sics_q), _p(sics_k), _p(as_q),
-                                         _p(as_k), _p(as_qk), _s(stream)))
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_aggregation_score, ctypes.byref(g),
+                 a(sics_q, F64, D.per_block, "sics_q"), a(sics_k, F64, D.per_block, "sics_k"),
+                 a(as_q, F64, D.per_head, "as_q"), a(as_k, F64, D.per_head, "as_k"),
+                 a(as_qk, F64, D.per_head, "as_qk"), stream))
 
 
 def spade_choose_scheme(as_qk, choice, best=None, stream=None):
     """as_qk: fp64 [C, B, H] device tensor; choice: int32 [H]; best: fp64 [H] or None."""
+    a = _Args()
     C, B, H = as_qk.shape
-    _check(lib().spade_choose_scheme(_p(as_qk), int(C), int(B), int(H), _p(choice), _p(best),
-                                     _s(stream)))
+    _check(a.run(lib().spade_choose_scheme, a(as_qk, F64, None, "as_qk"), int(C), int(B), int(H),
+                 a(choice, I32, H, "choice"), a(best, F64, H, "best"), stream))
 
 
 def spade_estimate_select(g: spade_geom, qbar, kbar, mode: int, topk: int, tau: float,
                           scale: float, counts, indices, scores=None, stream=None):
-    _check(lib().spade_estimate_select(ctypes.byref(g), _p(qbar), _p(kbar), int(mode), int(topk),
-                                       float(tau), float(scale), _p(counts), _p(indices),
-                                       _p(scores), _s(stream)))
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_estimate_select, ctypes.byref(g), a(qbar, F64, D.summ, "qbar"),
+                 a(kbar, F64, D.summ, "kbar"), int(mode), int(topk), float(tau), float(scale),
+                 a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
+                 a(scores, F64, D.pairs, "scores"), stream))
 
 
 def spade_block_minmax(g: spade_geom, q, k, qmax, qmin, kmax, kmin, sics_q=None, sics_k=None,
                        heads=None, stream=None):
+    a = _Args()
     arr, n = _head_list(heads)
-    _check(lib().spade_block_minmax(ctypes.byref(g), _p(q), _p(k), _p(qmax), _p(qmin), _p(kmax),
-                                    _p(kmin), _p(sics_q), _p(sics_k), arr, n, _s(stream)))
+    D = _Dims(g, n if heads is not None else None)
+    _check(a.run(lib().spade_block_minmax, ctypes.byref(g), a(q, BF16, D.raster, "q"),
+                 a(k, BF16, D.raster, "k"), a(qmax, F64, D.summ, "qmax"),
+                 a(qmin, F64, D.summ, "qmin"), a(kmax, F64, D.summ, "kmax"),
+                 a(kmin, F64, D.summ, "kmin"), a(sics_q, F64, D.per_block, "sics_q"),
+                 a(sics_k, F64, D.per_block, "sics_k"), arr, n, stream))
+
+
+def _value(p):
+    return None if p is None else p.value
 
 
 def mask_spec(estimator=SPADE_EST_MEAN, mode=SPADE_TOPK, topk=0, tau=1.0, scale=1.0,
@@ -193,46 +288,69 @@ def mask_spec(estimator=SPADE_EST_MEAN, mode=SPADE_TOPK, topk=0, tau=1.0, scale=
               intra_theta=0.0, window=(-1, -1, -1), sink_tokens=0) -> spade_mask_spec:
     """topk_per_head / tau_per_head: None or device tensors (int32 / fp64, [H]); the
     caller keeps them alive until the call has run on its stream."""
+    a = _Args()
+    tk = a(topk_per_head, I32, None, "topk_per_head")
+    tu = a(tau_per_head, F64, None, "tau_per_head")
+    a.ready()
     return spade_mask_spec(int(estimator), int(mode), int(topk), float(tau), float(scale),
-                           None if topk_per_head is None else topk_per_head.data_ptr(),
-                           None if tau_per_head is None else tau_per_head.data_ptr(),
-                           int(intra), int(intra_topk), float(intra_theta),
-                           (ctypes.c_int32 * 3)(*[int(w) for w in window]), int(sink_tokens))
+                           _value(tk), _value(tu), int(intra), int(intra_topk),
+                           float(intra_theta), (ctypes.c_int32 * 3)(*[int(w) for w in window]),
+                           int(sink_tokens))
 
 
 def summaries(qbar=None, kbar=None, qmax=None, qmin=None, kmax=None, kmin=None, sics_q=None,
               sics_k=None) -> spade_summaries:
-    ptr = lambda t: None if t is None else t.data_ptr()  # noqa: E731
-    return spade_summaries(ptr(qbar), ptr(kbar), ptr(qmax), ptr(qmin), ptr(kmax), ptr(kmin),
-                           ptr(sics_q), ptr(sics_k))
+    """Device fp64 summary tensors of one selection call (None: not given)."""
+    a = _Args()
+    ptrs = [_value(a(t, F64, None, name)) for t, name in (
+        (qbar, "qbar"), (kbar, "kbar"), (qmax, "qmax"), (qmin, "qmin"), (kmax, "kmax"),
+        (kmin, "kmin"), (sics_q, "sics_q"), (sics_k, "sics_k"))]
+    a.ready()
+    return spade_summaries(*ptrs)
 
 
 def spade_compose_select(g: spade_geom, spec: spade_mask_spec, summ: spade_summaries, counts,
                          indices, scores=None, stream=None):
-    _check(lib().spade_compose_select(ctypes.byref(g), ctypes.byref(spec), ctypes.byref(summ),
-                                      _p(counts), _p(indices), _p(scores), _s(stream)))
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_compose_select, ctypes.byref(g), ctypes.byref(spec),
+                 ctypes.byref(summ), a(counts, I32, D.per_block, "counts"),
+                 a(indices, I32, D.pairs, "indices"), a(scores, F64, D.pairs, "scores"),
+                 stream))
 
 
 def spade_sparse_attn_raster_multi(geoms, heads, q, k, v, scale: float, o, lse=None,
                                    workspace=None, stream=None):
     """geoms: sequence of spade_geom; heads: per head (scheme, counts, indices,
     counts_bstride, indices_bstride) with counts/indices device tensors (views at
-    batch 0 of the head)."""
+    batch 0 of the head, at least NB and NB*NB elements of its blocking)."""
+    a = _Args()
     ga = (spade_geom * len(geoms))(*geoms)
-    ha = (spade_head_lists * max(len(heads), 1))(
-        *[spade_head_lists(int(c), cn.data_ptr(), ix.data_ptr(), int(cs), int(xs))
-          for c, cn, ix, cs, xs in heads])
+    rows = []
+    for h, (c, cn, ix, cs, xs) in enumerate(heads):
+        nb = _Dims(geoms[int(c)]).NB if 0 <= int(c) < len(geoms) else None
+        pc = a(cn, I32, nb, f"heads[{h}] counts")
+        pi = a(ix, I32, None if nb is None else nb * nb, f"heads[{h}] indices")
+        rows.append(spade_head_lists(int(c), _value(pc), _value(pi), int(cs), int(xs)))
+    ha = (spade_head_lists * max(len(rows), 1))(*rows)
+    D = _Dims(geoms[0]) if len(geoms) else None
+    n_rast = D.raster if D else None
+    n_rows = D.raster_rows if D else None
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().spade_sparse_attn_raster_multi(ga, len(geoms), ha, _p(q), _p(k), _p(v),
-                                                float(scale), _p(o), _p(lse), _p(workspace),
-                                                nbytes, _s(stream)))
+    _check(a.run(lib().spade_sparse_attn_raster_multi, ga, len(geoms), ha,
+                 a(q, BF16, n_rast, "q"), a(k, BF16, n_rast, "k"), a(v, BF16, n_rast, "v"),
+                 float(scale), a(o, BF16, n_rast, "o"), a(lse, F32, n_rows, "lse"),
+                 a(workspace, None, None, "workspace"), nbytes, stream))
 
 
 def spade_policy_budgets(as_best, k_dyn: int, NB: int, k_out, heads=None, stream=None):
     """as_best: fp64 [H] device tensor; k_out: int32 [len(heads) or H] device tensor."""
+    a = _Args()
     arr, n = _head_list(heads)
-    _check(lib().spade_policy_budgets(_p(as_best), int(as_best.numel()), arr, n, int(k_dyn),
-                                      int(NB), _p(k_out), _s(stream)))
+    H = int(as_best.numel())
+    _check(a.run(lib().spade_policy_budgets, a(as_best, F64, None, "as_best"), H, arr, n,
+                 int(k_dyn), int(NB), a(k_out, I32, n if heads is not None else H, "k_out"),
+                 stream))
 
 
 def spade_attn_workspace_bytes(g: spade_geom) -> int:
@@ -241,15 +359,23 @@ def spade_attn_workspace_bytes(g: spade_geom) -> int:
 
 def spade_block_sparse_attn(g: spade_geom, qb, kb, vb, counts, indices, scale: float, ob,
                             lse=None, workspace=None, stream=None):
+    a = _Args()
+    D = _Dims(g)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().spade_block_sparse_attn(ctypes.byref(g), _p(qb), _p(kb), _p(vb), _p(counts),
-                                         _p(indices), float(scale), _p(ob), _p(lse),
-                                         _p(workspace), nbytes, _s(stream)))
+    _check(a.run(lib().spade_block_sparse_attn, ctypes.byref(g), a(qb, BF16, D.blocked, "qb"),
+                 a(kb, BF16, D.blocked, "kb"), a(vb, BF16, D.blocked, "vb"),
+                 a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
+                 float(scale), a(ob, BF16, D.blocked, "ob"), a(lse, F32, D.blocked_rows, "lse"),
+                 a(workspace, None, None, "workspace"), nbytes, stream))
 
 
 def spade_sparse_attn_raster(g: spade_geom, q, k, v, counts, indices, scale: float, o, lse=None,
                              workspace=None, stream=None):
+    a = _Args()
+    D = _Dims(g)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
-    _check(lib().spade_sparse_attn_raster(ctypes.byref(g), _p(q), _p(k), _p(v), _p(counts),
-                                          _p(indices), float(scale), _p(o), _p(lse),
-                                          _p(workspace), nbytes, _s(stream)))
+    _check(a.run(lib().spade_sparse_attn_raster, ctypes.byref(g), a(q, BF16, D.raster, "q"),
+                 a(k, BF16, D.raster, "k"), a(v, BF16, D.raster, "v"),
+                 a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
+                 float(scale), a(o, BF16, D.raster, "o"), a(lse, F32, D.raster_rows, "lse"),
+                 a(workspace, None, None, "workspace"), nbytes, stream))
