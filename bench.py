@@ -149,6 +149,17 @@ def cpu_baseline(Q, K, V, cfg, budget_s: float) -> dict:
             "seconds": round(t_sel_all + t_attn_all, 2)}
 
 
+def attn_kernel_label(g) -> str:
+    """Which attention kernel the library launches for this blocking: the paired
+    kernel for blocks of 5 row tiles (129..160 slots) whose 8-chunk ring and kept
+    list fit one CU's 160 KB of LDS, the single-member kernel otherwise."""
+    tiles = -(-g.bt * g.bh * g.bw // 32)
+    ring = 8 * 2 * 32 * g.d * 2
+    if tiles == 5 and ring + 256 * 4 + g.NB * 4 <= 160 * 1024:
+        return "spade attn_pp_kernel (paired waves, bf16 MFMA 32x32x16)"
+    return "spade attn_kernel (bf16 MFMA 32x32x16)"
+
+
 def traffic_record(kernel_file: str, workload_name: str):
     """HBM bytes per attention launch from committed rocprofv3 counters, if they
     were taken on the current kernel source; else None."""
@@ -429,7 +440,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic,
-                     "kernel": "spade attn_kernel (bf16 MFMA 32x32x16)",
+                     "kernel": attn_kernel_label(g),
                      "work_per_launch_tflop": round(kf / 1e12, 4)},
         "cpu_baseline": cpu,
         "stages": out_stages,

@@ -1,7 +1,13 @@
 // Flash block-sparse attention (paper Eq. (2), §3.3 optimisation (3)) on gfx950.
 //
-// One workgroup per query block (b, h, i); wave w owns query slots 32w..32w+31;
-// for most block sizes one more wave only issues the K/V loads.
+// One workgroup per query block (b, h, i). Two kernels share the data movement
+// and the math below:
+// - attn_kernel: wave w owns query slots 32w..32w+31; for most block sizes one
+//   more wave only issues the K/V loads.
+// - attn_pp_kernel, for blocks of 5 row tiles (129..160 slots): two waves per
+//   32-row tile split the kept walk (even / odd chunks) and alternate matrix and
+//   vector phases between barriers, so each SIMD overlaps one wave's MFMAs with
+//   the other's softmax; the pair merges by log-sum-exp.
 // Work items are dealt to the 8 XCDs so that all XCDs share one head at a time.
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
 // chunks of 32 key slots (only chunks that hold real keys).
@@ -230,35 +236,27 @@ __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, c
 // addressed through the blocking's slot -> token map, so no blocked copies exist.
 struct NoTable {};
 
-// MULTI (raster only): one launch over heads with different blockings; the work
-// item picks its head, and with it the geometry and block lists, from `tab`.
-template <int D, int W, bool LD, bool RASTER, bool MULTI>
-__global__ void __launch_bounds__(64 * (W + LD))
-    __attribute__((amdgpu_waves_per_eu(W + LD >= 3 ? 3 : 2)))
-    attn_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
-                const char* __restrict__ vb, const int* __restrict__ counts,
-                const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
-                float* __restrict__ lse, const int* __restrict__ order,
-                typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
-  using TL = Tile<D>;
-  __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
-  __shared__ int rel_raw[RASTER ? kMaxBS : 1];  // full-block slot -> raster token offset
-  extern __shared__ int list_raw[];  // kept list of this work item, NB entries
-  lds_char* const lds = (lds_char*)lds_raw;
-  lds_int* const list = (lds_int*)list_raw;
-  lds_int* const rel = (lds_int*)rel_raw;
-
-  // Workgroup w runs on XCD w % 8. Every XCD walks the heads in the same order
-  // and takes one contiguous eighth of each head's query blocks: the XCDs work
-  // on the same head at a time (its K/V stays in the MALL) and each XCD's L2
-  // serves spatially adjacent query blocks, whose kept K/V sets overlap.
-  // MULTI: the heads follow each other in the grid (per batch element), each
-  // padded to a multiple of 8 items, and are dealt to the XCDs the same way.
-  DevGeom g = g_arg;
+// The work item of a workgroup: its geometry, (batch, head) pair, query block i
+// (-1 for grid padding) and the source of its kept list.
+// Workgroup w runs on XCD w % 8. Every XCD walks the heads in the same order
+// and takes one contiguous eighth of each head's query blocks: the XCDs work
+// on the same head at a time (its K/V stays in the MALL) and each XCD's L2
+// serves spatially adjacent query blocks, whose kept K/V sets overlap.
+// MULTI: the heads follow each other in the grid (per batch element), each
+// padded to a multiple of 8 items, and are dealt to the XCDs the same way.
+struct Item {
+  DevGeom g;
   int64_t bh;
   int i;
   const int* cnt_src;
   const int* list_src;
+};
+
+template <bool MULTI, class Tab>
+__device__ __forceinline__ Item work_item(const DevGeom& g_arg, const int* counts,
+                                          const int* indices, const int* order, const Tab& tab) {
+  Item it;
+  it.g = g_arg;
   if constexpr (MULTI) {
     const int b = int(blockIdx.x) / tab.items_per_batch;
     const int w = int(blockIdx.x) - b * tab.items_per_batch;
@@ -279,24 +277,59 @@ __global__ void __launch_bounds__(64 * (W + LD))
       start = tab.head[k].start;
     }
     const MultiHead& mh = tab.head[k];
-    g = tab.geo[mh.geom];
+    it.g = tab.geo[mh.geom];
     const int local = w - start;  // same residue mod 8 as blockIdx.x
-    const int per_xcd = (g.NB + 7) / 8;
-    i = (local & 7) * per_xcd + (local >> 3);
-    if (i >= g.NB) return;
-    bh = int64_t(b) * g.H + mh.h;
-    cnt_src = mh.counts + int64_t(b) * mh.counts_bstride + i;
-    list_src = mh.indices + int64_t(b) * mh.indices_bstride + int64_t(i) * g.NB;
+    const int per_xcd = (it.g.NB + 7) / 8;
+    it.i = (local & 7) * per_xcd + (local >> 3);
+    if (it.i >= it.g.NB) {
+      it.i = -1;
+      return it;
+    }
+    it.bh = int64_t(b) * it.g.H + mh.h;
+    it.cnt_src = mh.counts + int64_t(b) * mh.counts_bstride + it.i;
+    it.list_src = mh.indices + int64_t(b) * mh.indices_bstride + int64_t(it.i) * it.g.NB;
   } else {
+    const DevGeom& g = it.g;
     const int per_xcd = (g.NB + 7) / 8;
     const int64_t slot = int64_t(blockIdx.x) >> 3;
-    bh = slot / per_xcd;
-    if (order) bh = order[bh];  // heads in the ranked order (heaviest first)
-    i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
-    if (i >= g.NB) return;  // grid padding when NB is not a multiple of 8
-    cnt_src = counts + bh * g.NB + i;
-    list_src = indices + (bh * g.NB + i) * int64_t(g.NB);
+    it.bh = slot / per_xcd;
+    if (order) it.bh = order[it.bh];  // heads in the ranked order (heaviest first)
+    it.i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
+    if (it.i >= g.NB) {  // grid padding when NB is not a multiple of 8
+      it.i = -1;
+      return it;
+    }
+    it.cnt_src = counts + it.bh * g.NB + it.i;
+    it.list_src = indices + (it.bh * g.NB + it.i) * int64_t(g.NB);
   }
+  return it;
+}
+
+// MULTI (raster only): one launch over heads with different blockings; the work
+// item picks its head, and with it the geometry and block lists, from `tab`.
+template <int D, int W, bool LD, bool RASTER, bool MULTI>
+__global__ void __launch_bounds__(64 * (W + LD))
+    __attribute__((amdgpu_waves_per_eu(W + LD >= 3 ? 3 : 2)))
+    attn_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
+                const char* __restrict__ vb, const int* __restrict__ counts,
+                const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
+                float* __restrict__ lse, const int* __restrict__ order,
+                typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
+  using TL = Tile<D>;
+  __shared__ __align__(16) char lds_raw[2 * TL::BUF_BYTES];
+  __shared__ int rel_raw[RASTER ? kMaxBS : 1];  // full-block slot -> raster token offset
+  extern __shared__ int list_raw[];  // kept list of this work item, NB entries
+  lds_char* const lds = (lds_char*)lds_raw;
+  lds_int* const list = (lds_int*)list_raw;
+  lds_int* const rel = (lds_int*)rel_raw;
+
+  const Item it = work_item<MULTI>(g_arg, counts, indices, order, tab);
+  if (it.i < 0) return;
+  const DevGeom g = it.g;
+  const int64_t bh = it.bh;
+  const int i = it.i;
+  const int* const cnt_src = it.cnt_src;
+  const int* const list_src = it.list_src;
   const BlockExt e_i = block_ext(g, i);
   const int n_i = e_i.n;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -516,6 +549,404 @@ __global__ void __launch_bounds__(64 * (W + LD))
   }
 }
 
+// Paired kernel (blocks of 5 row tiles, i.e. 129..160 slots). The waves of a
+// workgroup otherwise move through each chunk in step (LDS reads, S MFMAs,
+// softmax VALU, P.V MFMAs, barrier), so a SIMD's matrix and vector units take
+// turns instead of overlapping. Here each 32-row query tile has two compute
+// waves, placed on the same SIMD (waves w and w + 4 of a workgroup share one):
+// member A takes the even chunks of the kept walk, member B the odd ones, each
+// with its own online-softmax state, and the pair merges by log-sum-exp at the
+// end. A step has two halves separated by workgroup barriers:
+//   half 0: A runs P.V(2s-2) and S(2s) (MFMA), B the softmax of 2s-1 (VALU);
+//   half 1: B runs P.V(2s-1) and S(2s+1), A the softmax of 2s;
+// so on every SIMD one member's matrix work meets the other's vector work. Two
+// loader waves (even / odd chunks) keep an 8-chunk LDS ring three chunks ahead.
+// One workgroup (12 waves) fills a CU. With 4 row tiles the pairs would leave a
+// CU at 8 compute waves instead of 12, which is slower, so smaller blocks keep
+// the single-member kernel.
+constexpr int kRing = 8;
+constexpr int kPairTiles = 5;         // row tiles of the blocks the paired kernel takes
+constexpr int kPairLds = 160 * 1024;  // LDS of one CU, all of it for one workgroup
+
+template <int D>
+struct PPLayout {
+  static constexpr int RING_BYTES = kRing * Tile<D>::BUF_BYTES;
+  static constexpr int REL_OFF = RING_BYTES;
+  static constexpr int LIST_OFF = RING_BYTES + kMaxBS * 4;
+  static constexpr int LPC = 2 * Tile<D>::LOADS;  // loads per chunk (one loader wave)
+  static constexpr int MERGE_FLOATS = D / 32 * 16 + 2;  // per lane: O, m, l
+};
+
+// (tile, phase) of compute wave w of 2T: full octets pair w with w + 4.
+__device__ __forceinline__ void pp_role(int w, int T, int* tile, int* ph) {
+  const int full = (2 * T) / 8 * 8;
+  if (w < full) {
+    *tile = (w / 8) * 4 + (w & 3);
+    *ph = (w >> 2) & 1;
+  } else {
+    const int h = (2 * T - full) / 2, r = w - full;
+    *tile = full / 2 + r % h;
+    *ph = r >= h;
+  }
+}
+
+// wait until at most n chunks' loads (n = 0, 1, 2) of this wave are in flight
+template <int LPC>
+__device__ __forceinline__ void wait_chunks(int n) {
+  constexpr auto imm = [](int c) { return (c & 15) | (((c >> 4) & 3) << 14) | 0x70 | 0xF00; };
+  if (n <= 0)
+    __builtin_amdgcn_s_waitcnt(imm(0));
+  else if (n == 1)
+    __builtin_amdgcn_s_waitcnt(imm(LPC));
+  else
+    __builtin_amdgcn_s_waitcnt(imm(2 * LPC));
+}
+
+template <int D, int T, bool RASTER, bool MULTI>
+__global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_per_eu(3)))
+    attn_pp_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
+                   const char* __restrict__ vb, const int* __restrict__ counts,
+                   const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
+                   float* __restrict__ lse, const int* __restrict__ order,
+                   typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
+  using TL = Tile<D>;
+  using LY = PPLayout<D>;
+  constexpr int NT = 64 * (2 * T + 2);
+  extern __shared__ __align__(16) char smem_raw[];
+  lds_char* const lds = (lds_char*)smem_raw;
+  lds_int* const rel = (lds_int*)(smem_raw + LY::REL_OFF);
+  lds_int* const list = (lds_int*)(smem_raw + LY::LIST_OFF);
+
+  const Item it = work_item<MULTI>(g_arg, counts, indices, order, tab);
+  if (it.i < 0) return;
+  const DevGeom g = it.g;
+  const int64_t bh = it.bh;
+  const int i = it.i;
+  const BlockExt e_i = block_ext(g, i);
+  const int n_i = e_i.n;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool loader = wave >= 2 * T;
+  const int lp = wave - 2 * T;  // loader parity: 0 even chunks, 1 odd
+  int tile = T, ph = 0;          // loaders own no rows (32 T >= BS)
+  if (!loader) pp_role(wave, T, &tile, &ph);
+  tile = __builtin_amdgcn_readfirstlane(tile);
+  ph = __builtin_amdgcn_readfirstlane(ph);
+  const int q0 = tile * 32;
+  const int half = lane >> 5, r32 = lane & 31;
+  const int64_t head_row = RASTER ? bh * g.N : bh * g.NB * int64_t(g.BS);
+  auto q_row = [&](int qs) -> int64_t {
+    return RASTER ? head_row + ext_token(g, e_i, qs) : head_row + int64_t(i) * g.BS + qs;
+  };
+
+  bf16x8 qf[D / 16];
+  {
+    const int qs = q0 + r32;
+    const uint4* src = qb + q_row(min(qs, n_i - 1)) * TL::NCH + half;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (qs < n_i) v = src[2 * kk];
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const int cnt = min(max(*it.cnt_src, 0), g.NB);
+  for (int e = tid; e < cnt; e += NT) list[e] = it.list_src[e];
+  if (RASTER) {
+    for (int sl = tid; sl < g.BS; sl += NT) {
+      const int q = sl / g.bw;
+      rel[sl] = ((q / g.bh) * g.Hs + q % g.bh) * g.Ws + sl % g.bw;
+    }
+  }
+  __syncthreads();
+
+  // chunks of the kept walk (every wave computes the same count)
+  int nch = 0;
+  for (int e = lane; e < cnt; e += 64) {
+    const int j = list[e];
+    if (j >= 0 && j < g.NB) nch += (block_ext(g, j).n + kChunk - 1) / kChunk;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) nch += __shfl_xor(nch, off);
+  nch = __builtin_amdgcn_readfirstlane(nch);
+
+  const int v_row0 = 4 * ((lane >> 4) >> 1) + ((lane & 15) >> 2);
+  const int v_piece0 = 2 * ((lane >> 4) & 1) + (((lane & 15) & 3) >> 1);
+  const int v_sub = (lane & 1) * 8;
+  const int k_off = r32 * TL::ROW_BYTES;
+  const int k_sw = swz_k<D>(r32);
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
+  float m = -INFINITY, l = 0.0f;
+  const bool rows_live = !loader && q0 < n_i;
+  const bf16x2 ones = {__bf16(1.0f), __bf16(1.0f)};
+  const uint32_t lds_u32 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  auto kbuf = [&](int k) { return lds + (k & (kRing - 1)) * TL::BUF_BYTES; };
+
+  auto compute_s = [&](int k) {
+    lds_char* Kt = kbuf(k);
+    f32x16 sv;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sv[r] = 0.0f;
+    bf16x8 kf[D / 16];
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+      kf[kk] = *(lds_bf16x8*)(Kt + k_off + (((2 * kk + half) ^ k_sw) << 4));
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+      sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sv, 0, 0, 0);
+#pragma unroll
+    for (int gi = 0; gi < D / 32; ++gi) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    return sv;
+  };
+  bf16x8 p[2];
+  auto softmax = [&](f32x16 sv, int c0, int nj) {
+    if (c0 + kChunk > nj) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kr = (r >> 2) * 8 + 4 * half + (r & 3);
+        if (c0 + kr >= nj) sv[r] = -INFINITY;
+      }
+    }
+    float mx = sv[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sv[r]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+    }
+    if (__any(mx > m + kRescaleLog2)) {
+      const float mnew = fmaxf(m, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+      l *= alpha;
+#pragma unroll
+      for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+      m = mnew;
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[r], scale_log2, -m));
+      p[r >> 3][r & 7] = __bf16(e);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pr = {p[u][2 * e], p[u][2 * e + 1]};
+        l = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l, false);
+      }
+  };
+  auto pv = [&](int k) {
+    lds_char* Vt = kbuf(k) + TL::TILE_BYTES;
+    bf16x8 vf[D / 32][2];
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        bf16x4 h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int row = 16 * u + 8 * h + v_row0;
+          const int piece = (4 * t + v_piece0) ^ swz_v(row);
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
+        }
+        vf[t][u] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][u], p[u], o[t], 0, 0, 0);
+#pragma unroll
+    for (int gi = 0; gi < D / 64; ++gi) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
+    }
+  };
+
+  // One cursor per wave, on chunk 2s + par of step s (compute waves: their own
+  // chunk; loaders: three chunks ahead, the next one they issue).
+  const int par = loader ? lp : ph;
+  auto next2 = [&](Cursor c) { return next_chunk(g, list, cnt, next_chunk(g, list, cnt, c)); };
+  Cursor cur = next_chunk(g, list, cnt, {-1, 0, 0, -kChunk, e_i});
+  if (par == 1) cur = next_chunk(g, list, cnt, cur);
+  auto issue = [&](int k) {
+    loader_chunk<D, RASTER>(g, kb, vb, head_row, cur, rel,
+                            lds_u32 + (k & (kRing - 1)) * TL::BUF_BYTES, lane);
+  };
+  if (loader) {
+#pragma unroll 1
+    for (int r = 0; r < 3; ++r) {
+      if (par + 2 * r < nch) issue(par + 2 * r);
+      cur = next2(cur);
+    }
+    if (par == 0) wait_chunks<LY::LPC>((2 < nch) + (4 < nch));
+  }
+  const f32x16 zero16 = {};
+  const bf16x8 zero8 = {};
+  int sc0 = 0, snj = 0;  // first slot and real keys of the chunk whose S is held
+  f32x16 sv = zero16;
+  const int steps = nch > 0 ? (nch + 1) / 2 + 1 : 0;
+  // Each role runs its own loop (so S and P are never live across each other's
+  // phases); all three execute the same two barriers per step. In the matrix
+  // phase P.V of the previous own chunk runs before S of this one.
+  __syncthreads();
+  if (loader) {
+#pragma unroll 1
+    for (int st = 0; st < steps; ++st) {
+      const int k = 2 * st + par;
+      // half 0: loader 1 makes sure chunk 2s + 1 (read in half 1) has landed
+      if (par == 1 && k < nch) wait_chunks<LY::LPC>((k + 2 < nch) + (k + 4 < nch));
+      __syncthreads();
+      if (par == 0 && k + 6 < nch) issue(k + 6);  // slot of chunk 2s - 2, V read in half 0
+      // half 1: loader 0 makes sure chunk 2s + 2 (read in the next half 0) has landed
+      if (par == 0 && k + 2 < nch) wait_chunks<LY::LPC>((k + 4 < nch) + (k + 6 < nch));
+      __syncthreads();
+      if (par == 1 && k + 6 < nch) issue(k + 6);  // slot of chunk 2s - 1, V read in half 1
+      cur = next2(cur);
+    }
+  } else if (par == 0) {
+#pragma unroll 1
+    for (int st = 0; st < steps; ++st) {
+      const int k = 2 * st;
+      // half 0: matrix phase
+      if (rows_live && k >= 2 && k - 2 < nch) pv(k - 2);
+      if (rows_live && k < nch) {
+        sv = compute_s(k);
+        sc0 = cur.c0;
+        snj = cur.nj;
+      } else {
+        sv = zero16;
+      }
+      __syncthreads();
+      // half 1: vector phase
+      if (rows_live && k < nch) {
+        softmax(sv, sc0, snj);
+      } else {
+        p[0] = zero8;
+        p[1] = zero8;
+      }
+      __syncthreads();
+      cur = next2(cur);
+    }
+  } else {
+#pragma unroll 1
+    for (int st = 0; st < steps; ++st) {
+      const int k = 2 * st + 1;
+      // half 0: vector phase (the S computed in the previous step's half 1)
+      if (rows_live && k >= 2 && k - 2 < nch) {
+        softmax(sv, sc0, snj);
+      } else {
+        p[0] = zero8;
+        p[1] = zero8;
+      }
+      __syncthreads();
+      // half 1: matrix phase
+      if (rows_live && k >= 2 && k - 2 < nch) pv(k - 2);
+      if (rows_live && k < nch) {
+        sv = compute_s(k);
+        sc0 = cur.c0;
+        snj = cur.nj;
+      } else {
+        sv = zero16;
+      }
+      __syncthreads();
+      cur = next2(cur);
+    }
+  }
+
+  // merge: member B hands (O, m, l) to member A of its tile through LDS
+  float* mg = reinterpret_cast<float*>(smem_raw) + tile * (LY::MERGE_FLOATS * 64);
+  if (rows_live && ph == 1) {
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mg[(t * 16 + r) * 64 + lane] = o[t][r];
+    mg[(D / 32 * 16) * 64 + lane] = m;
+    mg[(D / 32 * 16 + 1) * 64 + lane] = l;
+  }
+  __syncthreads();
+  if (loader || ph == 1) return;
+  if (rows_live) {
+    const float mB = mg[(D / 32 * 16) * 64 + lane];
+    const float lB = mg[(D / 32 * 16 + 1) * 64 + lane];
+    const float mm = fmaxf(m, mB);
+    const bool none = mm == -INFINITY;
+    const float aA = none ? 0.0f : __builtin_amdgcn_exp2f(m - mm);
+    const float aB = none ? 0.0f : __builtin_amdgcn_exp2f(mB - mm);
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] = o[t][r] * aA + mg[(t * 16 + r) * 64 + lane] * aB;
+    l = l * aA + lB * aB;
+    m = mm;
+  }
+  {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l),
+                                                     false, false);
+    l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
+  const int qs = q0 + r32;
+  if (RASTER ? qs < n_i : qs < g.BS) {
+    const bool real = qs < n_i;
+    const float inv = (real && l > 0.0f) ? 1.0f / l : 0.0f;
+    const int64_t orow = real ? q_row(qs) : head_row + int64_t(i) * g.BS + qs;
+    __bf16* dst = ob + orow * D + 4 * half;
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = __bf16(o[t][4 * rq + e] * inv);
+        *reinterpret_cast<bf16x4*>(dst + 32 * t + 8 * rq) = v;
+      }
+    if (lse && real && half == 0)
+      lse[orow] = l > 0.0f ? (m + log2f(l)) * 0.69314718055994530942f : -INFINITY;
+  }
+}
+
+template <int D, int T, bool RASTER, bool MULTI>
+hipError_t launch_pp(const DevGeom& g, const void* qb, const void* kb, const void* vb,
+                     const int* counts, const int* indices, float scale_log2, void* ob,
+                     float* lse, hipStream_t s, const MultiTable* tab, const int* order,
+                     int nb_max) {
+  static bool attr_set = false;  // the ring and the kept list exceed the 64 KB default
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&attn_pp_kernel<D, T, RASTER, MULTI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, kPairLds);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  const size_t lds = size_t(PPLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int);
+  const uint4* q4 = static_cast<const uint4*>(qb);
+  const char* k1 = static_cast<const char*>(kb);
+  const char* v1 = static_cast<const char*>(vb);
+  __bf16* o2 = static_cast<__bf16*>(ob);
+  if constexpr (MULTI) {
+    const int64_t items = int64_t(g.B) * tab->items_per_batch;
+    attn_pp_kernel<D, T, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (2 * T + 2), lds, s>>>(
+        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, order, *tab);
+  } else {
+    const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
+    attn_pp_kernel<D, T, RASTER, MULTI><<<dim3(unsigned(items)), 64 * (2 * T + 2), lds, s>>>(
+        g, q4, k1, v1, counts, indices, scale_log2, o2, lse, order, NoTable{});
+  }
+  return hipGetLastError();
+}
+
 template <int D, int W, bool LD, bool RASTER, bool MULTI>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
@@ -552,6 +983,16 @@ template <int D, bool RASTER, bool MULTI = false>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                     hipStream_t s, const MultiTable* tab = nullptr, const int* order = nullptr) {
+  // the paired kernel for 5 row tiles when its ring and the kept list fit the LDS
+  int nb_max = g.NB;
+  if constexpr (MULTI) {
+    nb_max = 0;
+    for (int k = 0; k < tab->n_heads; ++k) nb_max = max(nb_max, tab->geo[tab->head[k].geom].NB);
+  }
+  if ((g.BS + 31) / 32 == kPairTiles &&
+      size_t(PPLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int) <= size_t(kPairLds))
+    return launch_pp<D, kPairTiles, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob,
+                                                   lse, s, tab, order, nb_max);
 #define SPADE_ATTN_CASE(w, ld)                                                                  \
   case w:                                                                                       \
     return launch_dw<D, w, ld, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob, \
