@@ -37,6 +37,9 @@ def _case(name):
         "w4_ragged": dict(T=7, Hs=12, Ws=21, bt=3, bh=5, bw=8, d=128, H=2),    # BS 120
         "w4_ragged_d64": dict(T=9, Hs=11, Ws=12, bt=4, bh=5, bw=5, d=64, H=2),  # BS 100
         "w6_ragged": dict(T=7, Hs=13, Ws=23, bt=3, bh=6, bw=10, d=128, H=2),   # BS 180
+        # paired-wave kernel (5 row tiles): ragged on every axis; a 5th tile of 8 rows
+        "pp_ragged_d64": dict(T=7, Hs=11, Ws=19, bt=4, bh=5, bw=8, d=64, H=2),  # BS 160
+        "pp_bs136": dict(T=5, Hs=19, Ws=16, bt=1, bh=17, bw=8, d=128, H=2),     # BS 136
     }
     kw = dict(table[name])
     return P.small_cfg(kw.pop("T"), kw.pop("Hs"), kw.pop("Ws"), kw.pop("bt"), kw.pop("bh"),
@@ -44,7 +47,7 @@ def _case(name):
 
 
 SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block",
-         "w4_ragged", "w4_ragged_d64", "w6_ragged"]
+         "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136"]
 
 
 def _say(*a):
@@ -173,7 +176,7 @@ def test_attention_on_oracle_mask(name):
     assert worst <= P.ATTN_MAX_ABS
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged_d64", "ragged_d128", "one_block"])
+@pytest.mark.parametrize("name", ["tiny", "ragged_d64", "ragged_d128", "one_block", "pp_ragged_d64"])
 def test_all_kept_equals_dense(name):
     """A full mask through the sparse kernel equals dense attention, Eq. (1)."""
     cfg = _case(name)
@@ -192,8 +195,9 @@ def test_all_kept_equals_dense(name):
     assert np.max(np.abs(P.to_np64(p.O) - ref)) <= P.ATTN_MAX_ABS
 
 
-def test_malformed_lists_are_clamped_and_skipped():
-    cfg = _case("ragged_d128")
+@pytest.mark.parametrize("name", ["ragged_d128", "bs144_tail"])
+def test_malformed_lists_are_clamped_and_skipped(name):
+    cfg = _case(name)
     og = P.geometry(cfg)
     NB = og.NB
     Q, K, V = P.bf16_inputs(cfg)

@@ -239,12 +239,17 @@ def test_sweep_full_hunyuan_shape():
     assert worst <= P.ATTN_MAX_ABS
 
 
-@pytest.mark.parametrize("case", ["small_d64", "small_d128_b2", "hunyuan"])
+@pytest.mark.parametrize("case", ["small_d64", "small_d128_b2", "small_pair_b2", "hunyuan"])
 def test_sweep_raster_multi_equals_grouped(case):
     """One multi-scheme raster call gives every head exactly the output of its
     group's blocked path (same rows, same arithmetic, same order)."""
     if case == "hunyuan":
         cfg, cands, sp = workload("hunyuan_sweep"), SWEEP_CANDIDATES, 0.85
+    elif case == "small_pair_b2":
+        # three 160-slot blockings (paired-wave kernel, different grids of blocks) beside a
+        # 120-slot one, two batch elements (the per-batch head ranking)
+        cfg = P.small_cfg(6, 15, 16, 1, 1, 1, d=64, H=4, B=2)
+        cands, sp = [(2, 5, 16), (4, 5, 8), (5, 4, 8), (3, 5, 8)], 0.6
     elif case == "small_d64":
         cfg = P.small_cfg(6, 16, 20, 1, 1, 1, d=64, H=6)
         cands, sp = [(2, 4, 4), (3, 4, 5), (2, 8, 2), (1, 16, 4)], 0.6
@@ -254,6 +259,9 @@ def test_sweep_raster_multi_equals_grouped(case):
     _say("raster multi sweep", case)
     Q, K, V = P.bf16_inputs(cfg)
     a = _sweep_path(cfg, cands, sp).run(Q, K, V)
-    b = _sweep_path(cfg, cands, sp, raster=True).run(Q, K, V)
+    pb = _sweep_path(cfg, cands, sp, raster=True)
+    b = pb.run(Q, K, V)
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    if case == "small_pair_b2":  # some head ran on a 160-slot blocking
+        assert any(int(c) < 3 for c in pb.choice.cpu())
