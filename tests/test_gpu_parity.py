@@ -195,6 +195,40 @@ def test_all_kept_equals_dense(name):
     assert np.max(np.abs(P.to_np64(p.O) - ref)) <= P.ATTN_MAX_ABS
 
 
+@pytest.mark.parametrize("name", ["ragged_d128", "w4_ragged", "bs144_tail", "pp_ragged_d64"])
+def test_extreme_logits_full_mask(name):
+    """Q and K scaled by 6 (logits ~36x larger, up to a few hundred): with every
+    block kept, each row's running max rises many times, so the online softmax's
+    rescale path (and, for 129..160-slot blocks, the pair merge) is exercised.
+    Reference: dense fp64 attention, Eq. (1), and its log-sum-exp."""
+    cfg = _case(name)
+    _say("extreme logits", name)
+    og = P.geometry(cfg)
+    Q, K, V = P.bf16_inputs(cfg)
+    Q, K = (Q.float() * 6).to(torch.bfloat16), (K.float() * 6).to(torch.bfloat16)
+    NB = og.NB
+    counts = np.full((cfg["B"], cfg["H"], NB), NB, np.int32)
+    idx = np.broadcast_to(np.arange(NB, dtype=np.int32), (cfg["B"], cfg["H"], NB, NB)).copy()
+    p = _path(cfg, with_lse=True)
+    p.reorder_in(Q, K, V)
+    p.attend(torch.from_numpy(counts).to(DEV), torch.from_numpy(idx).to(DEV))
+    p.restore()
+    torch.cuda.synchronize()
+    q, k, v = (P.to_np64(x) for x in (Q, K, V))
+    scale = P.scale_of(cfg["d"])
+    ref = O.dense_attention(q, k, v, scale)
+    logits = np.matmul(q, np.swapaxes(k, -1, -2)) * scale
+    mx = logits.max(axis=-1)
+    ref_lse = mx + np.log(np.exp(logits - mx[..., None]).sum(axis=-1))
+    assert float(mx.max()) > 100.0  # the inputs do reach large logits
+    err = float(np.max(np.abs(P.to_np64(p.O) - ref)))
+    _say(f"  max-abs {err:.3e}, largest logit {float(mx.max()):.1f}")
+    assert err <= P.ATTN_MAX_ABS
+    pos = O.token_position(og)
+    lse_raster = p.lse.cpu().numpy().astype(np.float64)[:, :, pos]
+    np.testing.assert_allclose(lse_raster, ref_lse, rtol=0, atol=P.LSE_MAX_ABS)
+
+
 @pytest.mark.parametrize("name", ["ragged_d128", "bs144_tail"])
 def test_malformed_lists_are_clamped_and_skipped(name):
     cfg = _case(name)
