@@ -293,8 +293,8 @@ def main():
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(the hot path shards by head with no exchange; see the design notes).",
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(the hot path would shard by head, with no exchange between GPUs).",
               file=sys.stderr)
         sys.exit(2)
     if not torch.cuda.is_available():
