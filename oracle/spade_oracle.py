@@ -22,8 +22,7 @@ paper's order (§3.3, Head-wise Sparse Attention):
 Plus the intra-block aggregation measure SICS, Eq. (4) and Eq. (5) / Alg. 1
 (§3.2), and the Aggregation Score, Eq. (3).
 
-Readings where the paper is silent (each is a stated choice, listed with the
-design notes):
+Readings where the paper is silent (each is a stated choice):
   * tokens are flattened T-major, n = (t*Hs + y)*Ws + x;
   * blocks are numbered T-major over the ceil-sized block grid; inside a block
     the valid tokens come first, in raster order of (dt, dy, dx); the remaining
