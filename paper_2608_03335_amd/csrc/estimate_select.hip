@@ -55,33 +55,67 @@ __device__ __forceinline__ uint64_t order_key(double s) {
   return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-  return v;
+// Wave-wide reductions without LDS round trips: DPP moves within each 16-lane row
+// (quad swaps, half-row and row mirrors: every lane ends with its row's total),
+// then the four row totals are read into scalar registers. Integer sums and
+// maxima are exact whatever the order.
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp32(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, ROW_MASK, BANK_MASK, true));
 }
+template <int CTRL, int ROW_MASK = 0xf, int BANK_MASK = 0xf>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+  return (uint64_t(dpp32<CTRL, ROW_MASK, BANK_MASK>(uint32_t(v >> 32))) << 32) |
+         dpp32<CTRL, ROW_MASK, BANK_MASK>(uint32_t(v));
+}
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+  return (uint64_t(uint32_t(__builtin_amdgcn_readlane(int(v >> 32), l))) << 32) |
+         uint32_t(__builtin_amdgcn_readlane(int(uint32_t(v)), l));
+}
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  return __longlong_as_double((long long)readlane64(uint64_t(__double_as_longlong(v)), l));
+}
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror
+constexpr int kDppSwap1 = 0xB1, kDppSwap2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t v) {
+  v += dpp64<kDppSwap1>(v);
+  v += dpp64<kDppSwap2>(v);
+  v += dpp64<kDppHalfMirror>(v);
+  v += dpp64<kDppMirror>(v);
+  return readlane64(v, 0) + readlane64(v, 16) + readlane64(v, 32) + readlane64(v, 48);
+}
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return a > b ? a : b; }
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    const uint64_t o = __shfl_xor(v, m, 64);
-    v = o > v ? o : v;
-  }
-  return v;
+  v = max_u64(v, dpp64<kDppSwap1>(v));
+  v = max_u64(v, dpp64<kDppSwap2>(v));
+  v = max_u64(v, dpp64<kDppHalfMirror>(v));
+  v = max_u64(v, dpp64<kDppMirror>(v));
+  return max_u64(max_u64(readlane64(v, 0), readlane64(v, 16)),
+                 max_u64(readlane64(v, 32), readlane64(v, 48)));
 }
 __device__ __forceinline__ double wave_max_f64(double v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) v = fmax(v, __shfl_xor(v, m, 64));
-  return v;
+  auto d = [](double x) { return uint64_t(__double_as_longlong(x)); };
+  v = fmax(v, __longlong_as_double((long long)dpp64<kDppSwap1>(d(v))));
+  v = fmax(v, __longlong_as_double((long long)dpp64<kDppSwap2>(d(v))));
+  v = fmax(v, __longlong_as_double((long long)dpp64<kDppHalfMirror>(d(v))));
+  v = fmax(v, __longlong_as_double((long long)dpp64<kDppMirror>(d(v))));
+  return fmax(fmax(readlane_f64(v, 0), readlane_f64(v, 16)),
+              fmax(readlane_f64(v, 32), readlane_f64(v, 48)));
 }
-// sum over lanes strictly above this one
+// sum over lanes strictly above this one: the wave's inclusive prefix sum by DPP
+// (row shifts 1, 2, 3 of the input, then 4 and 8 within the row, then the last lane
+// of row 0 into row 1 and 3, of row 1 into rows 2 and 3), subtracted from the total
 __device__ __forceinline__ uint64_t wave_suffix_excl_u64(uint64_t x, int lane) {
-  uint64_t v = x;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint64_t y = __shfl_down(v, off, 64);
-    if (lane + off < 64) v += y;
-  }
-  return v - x;
+  (void)lane;
+  uint64_t v = x + dpp64<0x111>(x);   // row_shr:1
+  v += dpp64<0x112>(x);               // row_shr:2
+  v += dpp64<0x113>(x);               // row_shr:3
+  v += dpp64<0x114, 0xf, 0xe>(v);     // row_shr:4, banks 1-3
+  v += dpp64<0x118, 0xf, 0xc>(v);     // row_shr:8, banks 2-3
+  v += dpp64<0x142, 0xa, 0xf>(v);     // row_bcast:15 into rows 1 and 3
+  v += dpp64<0x143, 0xc, 0xf>(v);     // row_bcast:31 into rows 2 and 3
+  return readlane64(v, 63) - v;
 }
 __device__ __forceinline__ int lanes_below(uint64_t ballot) {
   return __builtin_amdgcn_mbcnt_hi(uint32_t(ballot >> 32),
@@ -150,10 +184,10 @@ __device__ Cut find_cut(const uint64_t (&key)[SM], const uint64_t (&w)[SM], uint
         my_w = bw[q];
         my_c = bc[q];
       }
-    const int q_L = __shfl(bq, L, 64);
-    const uint64_t suf = __shfl(my_suf, L, 64);
-    const uint64_t wD = __shfl(my_w, L, 64);
-    const unsigned cD = __shfl(my_c, L, 64);
+    const int q_L = __builtin_amdgcn_readlane(bq, L);  // L is uniform (from a ballot)
+    const uint64_t suf = readlane64(my_suf, L);
+    const uint64_t wD = readlane64(my_w, L);
+    const unsigned cD = unsigned(__builtin_amdgcn_readlane(int(my_c), L));
     const int Dg = 4 * L + q_L;
     prefix |= uint64_t(Dg) << shift;
     if (cD == 1) {  // a single element in the bucket: its key is the cut
