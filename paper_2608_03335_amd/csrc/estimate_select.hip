@@ -132,18 +132,17 @@ struct Cut {
 
 // Radix search of one wave's keys (0 = no element) with weights w for the
 // largest t with W(key >= t) >= need. count_rule: the tie group fills the count
-// (Top-K); otherwise the mass (Top-P). hw/hc: this wave's LDS histograms.
+// (Top-K); otherwise the mass (Top-P). hw: this wave's LDS histogram of weights
+// (a bucket's element count, needed only to stop at a single element, comes from
+// ballots, so the contended LDS atomics are the weights' alone).
 template <int SM>
 __device__ Cut find_cut(const uint64_t (&key)[SM], const uint64_t (&w)[SM], uint64_t need,
-                        bool count_rule, uint64_t* hw, unsigned* hc, int lane) {
+                        bool count_rule, uint64_t* hw, int lane) {
   uint64_t prefix = 0, above = 0, tstar = 0;
   for (int pass = 0; pass < 8; ++pass) {
     const int shift = 56 - 8 * pass;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      hw[4 * lane + q] = 0;
-      hc[4 * lane + q] = 0;
-    }
+    for (int q = 0; q < 4; ++q) hw[4 * lane + q] = 0;
     wave_sync();
 #pragma unroll
     for (int s = 0; s < SM; ++s) {
@@ -152,17 +151,12 @@ __device__ Cut find_cut(const uint64_t (&key)[SM], const uint64_t (&w)[SM], uint
       if (cand) {
         const int dg = int((key[s] >> shift) & 255u);
         atomicAdd(reinterpret_cast<unsigned long long*>(&hw[dg]), (unsigned long long)w[s]);
-        atomicAdd(&hc[dg], 1u);
       }
     }
     wave_sync();
     uint64_t bw[4], loc[4];
-    unsigned bc[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      bw[q] = hw[4 * lane + q];
-      bc[q] = hc[4 * lane + q];
-    }
+    for (int q = 0; q < 4; ++q) bw[q] = hw[4 * lane + q];
     loc[3] = bw[3];
     loc[2] = loc[3] + bw[2];
     loc[1] = loc[2] + bw[1];
@@ -176,20 +170,21 @@ __device__ Cut find_cut(const uint64_t (&key)[SM], const uint64_t (&w)[SM], uint
     if (has == 0) return {0, 0, true};  // total weight below need
     const int L = 63 - __builtin_clzll(has);
     uint64_t my_suf = 0, my_w = 0;
-    unsigned my_c = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q)
       if (q == bq) {
         my_suf = E + loc[q];
         my_w = bw[q];
-        my_c = bc[q];
       }
     const int q_L = __builtin_amdgcn_readlane(bq, L);  // L is uniform (from a ballot)
     const uint64_t suf = readlane64(my_suf, L);
     const uint64_t wD = readlane64(my_w, L);
-    const unsigned cD = unsigned(__builtin_amdgcn_readlane(int(my_c), L));
     const int Dg = 4 * L + q_L;
     prefix |= uint64_t(Dg) << shift;
+    int cD = 0;  // elements in the chosen bucket
+#pragma unroll
+    for (int s = 0; s < SM; ++s)
+      cD += __popcll(__ballot(key[s] != 0 && (key[s] >> shift) == (prefix >> shift)));
     if (cD == 1) {  // a single element in the bucket: its key is the cut
       uint64_t kk = 0;
 #pragma unroll
@@ -251,7 +246,7 @@ __device__ __forceinline__ double coherence(const DevGeom& g, const double* sics
 // lo <= e < hi. One wave.
 template <int SM>
 __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, int lo, int hi,
-                                 unsigned char* mark, uint64_t* hw, unsigned* hc, int lane) {
+                                 unsigned char* mark, uint64_t* hw, int lane) {
   const int NB = g.NB;
   uint64_t key[SM], w[SM];
 #pragma unroll
@@ -260,7 +255,7 @@ __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, in
     key[s] = e < NB ? order_key(-coherence(g, sics, e) + 0.0) : 0;  // least coherent first
     w[s] = key[s] != 0 ? 1 : 0;
   }
-  const Cut c = find_cut<SM>(key, w, uint64_t(min(k, NB)), true, hw, hc, lane);
+  const Cut c = find_cut<SM>(key, w, uint64_t(min(k, NB)), true, hw, lane);
   int tie_base = 0;
 #pragma unroll
   for (int s = 0; s < SM; ++s) {
@@ -284,8 +279,7 @@ __global__ void __launch_bounds__(kThreads)
   const int NB = g.NB;
   double* sc = reinterpret_cast<double*>(smem);                           // [kRows][NB]
   uint64_t* hist_w = reinterpret_cast<uint64_t*>(sc + kRows * NB);         // [kWaves][256]
-  unsigned* hist_c = reinterpret_cast<unsigned*>(hist_w + kWaves * 256);  // [kWaves][256]
-  int* coord = reinterpret_cast<int*>(hist_c + kWaves * 256);             // [NB]
+  int* coord = reinterpret_cast<int*>(hist_w + kWaves * 256);             // [NB]
   unsigned char* colmark = reinterpret_cast<unsigned char*>(coord + NB);  // [NB]
   unsigned char* rowmark = colmark + NB;                                  // [kRows]
 
@@ -416,18 +410,16 @@ __global__ void __launch_bounds__(kThreads)
   __syncthreads();
   if (p.intra == kIntraTopk && p.intra_k > 0) {
     if (wave == 0)
-      intra_topk_marks<SM>(g, p.sics_k + bh * NB, p.intra_k, 0, NB, colmark, hist_w, hist_c,
-                           lane);
+      intra_topk_marks<SM>(g, p.sics_k + bh * NB, p.intra_k, 0, NB, colmark, hist_w, lane);
     else if (wave == 1)
       intra_topk_marks<SM>(g, p.sics_q + bh * NB, p.intra_k, i0, i0 + kRows, rowmark,
-                           hist_w + 256, hist_c + 256, lane);
+                           hist_w + 256, lane);
     __syncthreads();
   }
 
   // ---------------- phase 2: one wave per row ----------------
   const int S = (NB + 63) / 64;
   uint64_t* hw = hist_w + wave * 256;
-  unsigned* hc = hist_c + wave * 256;
   const int topk = p.topk_h ? min(max(p.topk_h[h], 1), NB) : p.topk;
   const double tau = p.tau_h ? p.tau_h[h] : p.tau;
   for (int rr = wave; rr < kRows; rr += kWaves) {
@@ -477,7 +469,7 @@ __global__ void __launch_bounds__(kThreads)
       need = uint64_t(ceil(t * double(z)));
       need = need < 1 ? 1 : (need > z ? z : need);
     }
-    const Cut c = find_cut<SM>(key, w, need, p.mode == 0, hw, hc, lane);
+    const Cut c = find_cut<SM>(key, w, need, p.mode == 0, hw, lane);
 
     int cnt_out = 0;
     if (c.all) {
@@ -507,14 +499,14 @@ __global__ void __launch_bounds__(kThreads)
 
 template <int D, int EST, int SM>
 hipError_t launch_des(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
-  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * (8 + 4) +
+  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * 8 +
                      size_t(g.NB) * (4 + 1) + kRows;
   static bool attr_set = false;  // raising the dynamic-LDS cap once is idempotent
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(
         reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
         hipFuncAttributeMaxDynamicSharedMemorySize,
-        int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 12 + kMaxSelectNB * 5 + kRows));
+        int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 8 + kMaxSelectNB * 5 + kRows));
     if (e != hipSuccess) return e;
     attr_set = true;
   }
