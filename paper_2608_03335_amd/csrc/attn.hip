@@ -8,7 +8,8 @@
 //   32-row tile split the kept walk (even / odd chunks) and alternate matrix and
 //   vector phases between barriers, so each SIMD overlaps one wave's MFMAs with
 //   the other's softmax; the pair merges by log-sum-exp.
-// Work items are dealt to the 8 XCDs so that all XCDs share one head at a time.
+// Work items are dealt to the 8 XCDs so that all XCDs share one head at a time;
+// each XCD starts its rows of a head heaviest first (heavy_first).
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
 // chunks of 32 key slots (only chunks that hold real keys).
 //
@@ -252,6 +253,25 @@ struct Item {
   const int* list_src;
 };
 
+// Row of rank r among the n query blocks c[0..n) of one XCD's share of a head, ordered
+// by kept-block count (descending, ties to the lower index) within windows of 64. The
+// XCD's CUs then start its rows heaviest first: rows of similar length walk the key
+// blocks at a similar pace, so the K/V blocks they share meet in the XCD's L2, and long
+// rows do not form the tail. Any order is correct: each row is one work item.
+__device__ __forceinline__ int heavy_first(const int* __restrict__ c, int n, int r, int NB) {
+  const int lane = int(threadIdx.x & 63);
+  const int w0 = r & ~63, wn = min(64, n - w0);
+  const int cl = min(max(c[w0 + min(lane, wn - 1)], 0), NB);  // lanes past the window re-read
+  const int key = lane < wn ? cl : -1;
+  int rank = 0;
+  for (int t = 0; t < wn; ++t) {
+    const int kt = __builtin_amdgcn_readlane(key, t);
+    rank += (kt > key || (kt == key && t < lane)) ? 1 : 0;
+  }
+  const uint64_t hit = __ballot(lane < wn && rank == r - w0);
+  return w0 + __builtin_amdgcn_readfirstlane(int(__builtin_ctzll(hit)));
+}
+
 template <bool MULTI, class Tab>
 __device__ __forceinline__ Item work_item(const DevGeom& g_arg, const int* counts,
                                           const int* indices, const int* order, const Tab& tab) {
@@ -280,13 +300,16 @@ __device__ __forceinline__ Item work_item(const DevGeom& g_arg, const int* count
     it.g = tab.geo[mh.geom];
     const int local = w - start;  // same residue mod 8 as blockIdx.x
     const int per_xcd = (it.g.NB + 7) / 8;
-    it.i = (local & 7) * per_xcd + (local >> 3);
-    if (it.i >= it.g.NB) {
+    const int lo = (local & 7) * per_xcd, r = local >> 3;
+    const int rows = min(per_xcd, it.g.NB - lo);
+    if (r >= rows) {
       it.i = -1;
       return it;
     }
+    const int* hc = mh.counts + int64_t(b) * mh.counts_bstride;
+    it.i = lo + heavy_first(hc + lo, rows, r, it.g.NB);
     it.bh = int64_t(b) * it.g.H + mh.h;
-    it.cnt_src = mh.counts + int64_t(b) * mh.counts_bstride + it.i;
+    it.cnt_src = hc + it.i;
     it.list_src = mh.indices + int64_t(b) * mh.indices_bstride + int64_t(it.i) * it.g.NB;
   } else {
     const DevGeom& g = it.g;
@@ -294,11 +317,13 @@ __device__ __forceinline__ Item work_item(const DevGeom& g_arg, const int* count
     const int64_t slot = int64_t(blockIdx.x) >> 3;
     it.bh = slot / per_xcd;
     if (order) it.bh = order[it.bh];  // heads in the ranked order (heaviest first)
-    it.i = int(blockIdx.x & 7) * per_xcd + int(slot % per_xcd);
-    if (it.i >= g.NB) {  // grid padding when NB is not a multiple of 8
+    const int lo = int(blockIdx.x & 7) * per_xcd, r = int(slot % per_xcd);
+    const int rows = min(per_xcd, g.NB - lo);
+    if (r >= rows) {  // grid padding when NB is not a multiple of 8
       it.i = -1;
       return it;
     }
+    it.i = lo + heavy_first(counts + it.bh * g.NB + lo, rows, r, g.NB);
     it.cnt_src = counts + it.bh * g.NB + it.i;
     it.list_src = indices + (it.bh * g.NB + it.i) * int64_t(g.NB);
   }
@@ -746,9 +771,13 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
         l = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, l, false);
       }
   };
-  auto pv = [&](int k) {
+  // V^T fragments of a chunk are read at the end of the vector phase that made its P
+  // (S is dead by then), so the matrix phase starts on MFMAs instead of an LDS round
+  // trip; they stay in registers across the barrier.
+  bf16x8 vf[D / 32][2];
+  auto read_v = [&](int k) {
+    __builtin_amdgcn_sched_barrier(0);
     lds_char* Vt = kbuf(k) + TL::TILE_BYTES;
-    bf16x8 vf[D / 32][2];
 #pragma unroll
     for (int t = 0; t < D / 32; ++t)
 #pragma unroll
@@ -763,16 +792,13 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
         }
         vf[t][u] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
       }
+  };
+  auto pv = [&]() {
 #pragma unroll
     for (int t = 0; t < D / 32; ++t)
 #pragma unroll
       for (int u = 0; u < 2; ++u)
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][u], p[u], o[t], 0, 0, 0);
-#pragma unroll
-    for (int gi = 0; gi < D / 64; ++gi) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 8, 1);
-      __builtin_amdgcn_sched_group_barrier(0x008, 4, 1);
-    }
   };
 
   // One cursor per wave, on chunk 2s + par of step s (compute waves: their own
@@ -800,7 +826,8 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
   const int steps = nch > 0 ? (nch + 1) / 2 + 1 : 0;
   // Each role runs its own loop (so S and P are never live across each other's
   // phases); all three execute the same two barriers per step. In the matrix
-  // phase P.V of the previous own chunk runs before S of this one.
+  // phase P.V of the previous own chunk (its V^T already in registers) runs before
+  // S of this one.
   __syncthreads();
   if (loader) {
 #pragma unroll 1
@@ -821,7 +848,7 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
     for (int st = 0; st < steps; ++st) {
       const int k = 2 * st;
       // half 0: matrix phase
-      if (rows_live && k >= 2 && k - 2 < nch) pv(k - 2);
+      if (rows_live && k >= 2 && k - 2 < nch) pv();
       if (rows_live && k < nch) {
         sv = compute_s(k);
         sc0 = cur.c0;
@@ -833,9 +860,12 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
       // half 1: vector phase
       if (rows_live && k < nch) {
         softmax(sv, sc0, snj);
+        read_v(k);
       } else {
         p[0] = zero8;
         p[1] = zero8;
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t) vf[t][0] = vf[t][1] = zero8;
       }
       __syncthreads();
       cur = next2(cur);
@@ -847,13 +877,16 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
       // half 0: vector phase (the S computed in the previous step's half 1)
       if (rows_live && k >= 2 && k - 2 < nch) {
         softmax(sv, sc0, snj);
+        read_v(k - 2);
       } else {
         p[0] = zero8;
         p[1] = zero8;
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t) vf[t][0] = vf[t][1] = zero8;
       }
       __syncthreads();
       // half 1: matrix phase
-      if (rows_live && k >= 2 && k - 2 < nch) pv(k - 2);
+      if (rows_live && k >= 2 && k - 2 < nch) pv();
       if (rows_live && k < nch) {
         sv = compute_s(k);
         sc0 = cur.c0;
@@ -1011,7 +1044,7 @@ hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void
 // similar density co-scheduled). The dispatch walks the (batch, head) pairs in
 // the order of their heaviest row, then their total kept blocks (descending,
 // ties to the lower index), so long rows start first instead of forming the
-// tail; within a head the XCD mapping is unchanged.
+// tail; within a head each XCD takes its rows heaviest first (heavy_first).
 constexpr int kRankThreads = 1024;
 constexpr int kMaxRankedHeads = 4096;  // beyond this many (batch, head) pairs: grid order
 
