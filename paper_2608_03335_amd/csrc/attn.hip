@@ -833,14 +833,16 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
 #pragma unroll 1
     for (int st = 0; st < steps; ++st) {
       const int k = 2 * st + par;
-      // half 0: loader 1 makes sure chunk 2s + 1 (read in half 1) has landed
+      // half 0: loader 0 refills the slot of chunk 2s - 2 (its V^T was read in the
+      // previous half 1); loader 1 makes sure chunk 2s + 1 (read in half 1) has landed
+      if (par == 0 && k + 6 < nch) issue(k + 6);
       if (par == 1 && k < nch) wait_chunks<LY::LPC>((k + 2 < nch) + (k + 4 < nch));
       __syncthreads();
-      if (par == 0 && k + 6 < nch) issue(k + 6);  // slot of chunk 2s - 2, V read in half 0
-      // half 1: loader 0 makes sure chunk 2s + 2 (read in the next half 0) has landed
+      // half 1: loader 1 refills the slot of chunk 2s - 1 (V^T read in half 0); loader 0
+      // makes sure chunk 2s + 2 (read in the next half 0) has landed
+      if (par == 1 && k + 6 < nch) issue(k + 6);
       if (par == 0 && k + 2 < nch) wait_chunks<LY::LPC>((k + 4 < nch) + (k + 6 < nch));
       __syncthreads();
-      if (par == 1 && k + 6 < nch) issue(k + 6);  // slot of chunk 2s - 1, V read in half 1
       cur = next2(cur);
     }
   } else if (par == 0) {
