@@ -189,6 +189,11 @@ __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, con
 // full blocks) and the offset carries the slot's raster token (the head's rows
 // span < 2^31 bytes, checked on the host); a lane's K and V rows are the same,
 // so each offset is computed once.
+template <int D>
+__device__ __forceinline__ void loader_issue(const char* kb, const char* vb, int64_t base_row,
+                                             const uint32_t (&row_off)[Tile<D>::LOADS],
+                                             uint32_t lds_buf, int lane);
+
 template <int D, bool RASTER>
 __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, const char* vb,
                                              int64_t head_row, const Cursor& c, const lds_int* rel,
@@ -213,6 +218,16 @@ __device__ __forceinline__ void loader_chunk(const DevGeom& g, const char* kb, c
     else
       fill([&](int sr) { return int(ext_token(g, c.e, c.c0 + sr)); });
   }
+  loader_issue<D>(kb, vb, base_row, row_off, lds_buf, lane);
+}
+
+// The 2*LOADS wave-wide DMA loads of one chunk: K and V rows at base_row + the lane's
+// row offsets (bytes), into the chunk's LDS buffer.
+template <int D>
+__device__ __forceinline__ void loader_issue(const char* kb, const char* vb, int64_t base_row,
+                                             const uint32_t (&row_off)[Tile<D>::LOADS],
+                                             uint32_t lds_buf, int lane) {
+  using TL = Tile<D>;
   const char* kbase = kb + base_row * TL::ROW_BYTES;
   const char* vbase = vb + base_row * TL::ROW_BYTES;
 #pragma unroll
@@ -830,17 +845,46 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
   // S of this one.
   __syncthreads();
   if (loader) {
+    // Raster layout: the row offsets of a full block's chunk depend only on the
+    // chunk's position in the block (T positions), so they are read from the slot
+    // table once here; the loop then issues full-block chunks without LDS reads,
+    // which would queue behind the compute waves' K and V^T reads.
+    uint32_t pre[RASTER ? T : 1][TL::LOADS];
+    if (RASTER) {
+#pragma unroll
+      for (int ps = 0; ps < T; ++ps)
+#pragma unroll
+        for (int qq = 0; qq < TL::LOADS; ++qq) {
+          const int sr = min(qq * TL::RPI + lane / TL::NCH, max(g.BS - 1 - ps * kChunk, 0));
+          pre[ps][qq] = uint32_t(rel[min(ps * kChunk + sr, g.BS - 1)] * TL::ROW_BYTES);
+        }
+    }
+    auto issue_loop = [&](int k) {
+      const uint32_t buf = lds_u32 + (k & (kRing - 1)) * TL::BUF_BYTES;
+      if (RASTER && cur.e.n == g.BS) {
+        uint32_t ro[TL::LOADS];
+        const int ps = cur.c0 / kChunk;
+#pragma unroll
+        for (int pp = 0; pp < T; ++pp)
+          if (pp == ps)
+#pragma unroll
+            for (int qq = 0; qq < TL::LOADS; ++qq) ro[qq] = pre[RASTER ? pp : 0][qq];
+        loader_issue<D>(kb, vb, head_row + block_origin(g, cur.e), ro, buf, lane);
+      } else {
+        loader_chunk<D, RASTER>(g, kb, vb, head_row, cur, rel, buf, lane);
+      }
+    };
 #pragma unroll 1
     for (int st = 0; st < steps; ++st) {
       const int k = 2 * st + par;
       // half 0: loader 0 refills the slot of chunk 2s - 2 (its V^T was read in the
       // previous half 1); loader 1 makes sure chunk 2s + 1 (read in half 1) has landed
-      if (par == 0 && k + 6 < nch) issue(k + 6);
+      if (par == 0 && k + 6 < nch) issue_loop(k + 6);
       if (par == 1 && k < nch) wait_chunks<LY::LPC>((k + 2 < nch) + (k + 4 < nch));
       __syncthreads();
       // half 1: loader 1 refills the slot of chunk 2s - 1 (V^T read in half 0); loader 0
       // makes sure chunk 2s + 2 (read in the next half 0) has landed
-      if (par == 1 && k + 6 < nch) issue(k + 6);
+      if (par == 1 && k + 6 < nch) issue_loop(k + 6);
       if (par == 0 && k + 2 < nch) wait_chunks<LY::LPC>((k + 4 < nch) + (k + 6 < nch));
       __syncthreads();
       cur = next2(cur);
