@@ -40,6 +40,9 @@ def _case(name):
         # paired-wave kernel (5 row tiles): ragged on every axis; a 5th tile of 8 rows
         "pp_ragged_d64": dict(T=7, Hs=11, Ws=19, bt=4, bh=5, bw=8, d=64, H=2),  # BS 160
         "pp_bs136": dict(T=5, Hs=19, Ws=16, bt=1, bh=17, bw=8, d=128, H=2),     # BS 136
+        # NB 1000 (ragged), near the selection limit: 125 query blocks per XCD share,
+        # so the heaviest-first ranking of work items runs over two windows of 64 rows
+        "many_blocks": dict(T=4, Hs=19, Ws=49, bt=1, bh=2, bw=2, d=64, H=2),   # BS 4
     }
     kw = dict(table[name])
     return P.small_cfg(kw.pop("T"), kw.pop("Hs"), kw.pop("Ws"), kw.pop("bt"), kw.pop("bh"),
@@ -47,7 +50,7 @@ def _case(name):
 
 
 SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block",
-         "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136"]
+         "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136", "many_blocks"]
 
 
 def _say(*a):
