@@ -597,10 +597,12 @@ __global__ void __launch_bounds__(64 * (W + LD))
 // member A takes the even chunks of the kept walk, member B the odd ones, each
 // with its own online-softmax state, and the pair merges by log-sum-exp at the
 // end. A step has two halves separated by workgroup barriers:
-//   half 0: A runs P.V(2s-2) and S(2s) (MFMA), B the softmax of 2s-1 (VALU);
-//   half 1: B runs P.V(2s-1) and S(2s+1), A the softmax of 2s;
+//   half 0: A runs P.V(2s-2) and S(2s) (MFMA), B the softmax of 2s-1 (VALU) and
+//           reads the V^T fragments of 2s-1 into registers;
+//   half 1: B runs P.V(2s-1) and S(2s+1), A the softmax of 2s and its V^T reads;
 // so on every SIMD one member's matrix work meets the other's vector work. Two
-// loader waves (even / odd chunks) keep an 8-chunk LDS ring three chunks ahead.
+// loader waves (even / odd chunks) keep an 8-chunk LDS ring three chunks ahead;
+// a slot is refilled in the half after its V^T was read.
 // One workgroup (12 waves) fills a CU. With 4 row tiles the pairs would leave a
 // CU at 8 compute waves instead of 12, which is slower, so smaller blocks keep
 // the single-member kernel.
