@@ -614,7 +614,8 @@ template <int D>
 struct PPLayout {
   static constexpr int RING_BYTES = kRing * Tile<D>::BUF_BYTES;
   static constexpr int REL_OFF = RING_BYTES;
-  static constexpr int LIST_OFF = RING_BYTES + kMaxBS * 4;
+  static constexpr int KVAL_OFF = RING_BYTES + kMaxBS * 4;  // real keys per ring slot
+  static constexpr int LIST_OFF = KVAL_OFF + kRing * 4;
   static constexpr int LPC = 2 * Tile<D>::LOADS;  // loads per chunk (one loader wave)
   static constexpr int MERGE_FLOATS = D / 32 * 16 + 2;  // per lane: O, m, l
 };
@@ -658,6 +659,7 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
   lds_char* const lds = (lds_char*)smem_raw;
   lds_int* const rel = (lds_int*)(smem_raw + LY::REL_OFF);
   lds_int* const list = (lds_int*)(smem_raw + LY::LIST_OFF);
+  lds_int* const kval = (lds_int*)(smem_raw + LY::KVAL_OFF);
 
   const Item it = work_item<MULTI>(g_arg, counts, indices, order, tab);
   if (it.i < 0) return;
@@ -818,13 +820,21 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
         o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][u], p[u], o[t], 0, 0, 0);
   };
 
-  // One cursor per wave, on chunk 2s + par of step s (compute waves: their own
-  // chunk; loaders: three chunks ahead, the next one they issue).
+  // Loaders keep a cursor on chunk 2s + par of step s, three chunks ahead (the next
+  // one they issue), and record each chunk's real keys beside its ring slot, so the
+  // compute waves mask without walking the kept list themselves.
   const int par = loader ? lp : ph;
   auto next2 = [&](Cursor c) { return next_chunk(g, list, cnt, next_chunk(g, list, cnt, c)); };
-  Cursor cur = next_chunk(g, list, cnt, {-1, 0, 0, -kChunk, e_i});
-  if (par == 1) cur = next_chunk(g, list, cnt, cur);
+  Cursor cur{};
+  if (loader) {
+    cur = next_chunk(g, list, cnt, {-1, 0, 0, -kChunk, e_i});
+    if (par == 1) cur = next_chunk(g, list, cnt, cur);
+  }
+  auto record = [&](int k) {
+    if (lane == 0) kval[k & (kRing - 1)] = min(cur.nj - cur.c0, kChunk);
+  };
   auto issue = [&](int k) {
+    record(k);
     loader_chunk<D, RASTER>(g, kb, vb, head_row, cur, rel,
                             lds_u32 + (k & (kRing - 1)) * TL::BUF_BYTES, lane);
   };
@@ -838,7 +848,8 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
   }
   const f32x16 zero16 = {};
   const bf16x8 zero8 = {};
-  int sc0 = 0, snj = 0;  // first slot and real keys of the chunk whose S is held
+  const int sc0 = 0;  // the held S covers keys 0 .. snj - 1 of its chunk
+  int snj = 0;
   f32x16 sv = zero16;
   const int steps = nch > 0 ? (nch + 1) / 2 + 1 : 0;
   // Each role runs its own loop (so S and P are never live across each other's
@@ -862,6 +873,7 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
         }
     }
     auto issue_loop = [&](int k) {
+      record(k);
       const uint32_t buf = lds_u32 + (k & (kRing - 1)) * TL::BUF_BYTES;
       if (RASTER && cur.e.n == g.BS) {
         uint32_t ro[TL::LOADS];
@@ -899,8 +911,7 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
       if (rows_live && k >= 2 && k - 2 < nch) pv();
       if (rows_live && k < nch) {
         sv = compute_s(k);
-        sc0 = cur.c0;
-        snj = cur.nj;
+        snj = kval[k & (kRing - 1)];
       } else {
         sv = zero16;
       }
@@ -916,7 +927,6 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
         for (int t = 0; t < D / 32; ++t) vf[t][0] = vf[t][1] = zero8;
       }
       __syncthreads();
-      cur = next2(cur);
     }
   } else {
 #pragma unroll 1
@@ -937,13 +947,11 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
       if (rows_live && k >= 2 && k - 2 < nch) pv();
       if (rows_live && k < nch) {
         sv = compute_s(k);
-        sc0 = cur.c0;
-        snj = cur.nj;
+        snj = kval[k & (kRing - 1)];
       } else {
         sv = zero16;
       }
       __syncthreads();
-      cur = next2(cur);
     }
   }
 
