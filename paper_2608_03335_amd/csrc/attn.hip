@@ -71,7 +71,11 @@ struct Tile {
 // swizzles: LDS piece c of tile row r holds global piece c ^ f(r)
 template <int D>
 __device__ __forceinline__ int swz_k(int r) { return r & (Tile<D>::NCH - 1); }
-__device__ __forceinline__ int swz_v(int r) { return 2 * (r & 3); }
+// V: in a transposing read, lanes 0-15 take pieces 4t + {0,1} and lanes 16-31 pieces
+// 4t + {2,3} of rows 0-3; an XOR stride of 4 pieces (d = 128) keeps the two groups'
+// pieces disjoint, so 32 lanes hit 64 distinct banks (no LDS bank conflicts)
+template <int D>
+__device__ __forceinline__ int swz_v(int r) { return D >= 128 ? 4 * (r & 3) : 2 * (r & 3); }
 
 // Position in the kept-block walk: list entry jj, its block j and real-key count nj,
 // the chunk's first key slot c0, and block j's extent (raster addressing).
@@ -173,7 +177,7 @@ __device__ __forceinline__ void load_chunk(const DevGeom& g, const char* kb, con
       const bool is_v = q >= TL::LOADS;
       const int qq = is_v ? q - TL::LOADS : q;
       const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
-      const int gp = piece ^ (is_v ? swz_v(r) : swz_k<D>(r));
+      const int gp = piece ^ (is_v ? swz_v<D>(r) : swz_k<D>(r));
       const char* src = (is_v ? vb : kb) + (base + rows[k]) * TL::ROW_BYTES + gp * 16;
       const uint32_t dst =  // M0: LDS base of this wave-wide 1 KB load
           uint32_t(reinterpret_cast<uintptr_t>(buf)) + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;
@@ -235,7 +239,7 @@ __device__ __forceinline__ void loader_issue(const char* kb, const char* vb, int
     const bool is_v = q >= TL::LOADS;
     const int qq = is_v ? q - TL::LOADS : q;
     const int r = qq * TL::RPI + lane / TL::NCH;  // tile row (key slot in chunk)
-    const int gp = (lane % TL::NCH) ^ (is_v ? swz_v(r) : swz_k<D>(r));
+    const int gp = (lane % TL::NCH) ^ (is_v ? swz_v<D>(r) : swz_k<D>(r));
     const uint32_t off = row_off[qq] + uint32_t(gp * 16);
     const uint32_t dst = lds_buf + (is_v ? TL::TILE_BYTES : 0) + qq * 1024;  // M0
     asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(is_v ? vbase : kbase),
@@ -537,7 +541,7 @@ __global__ void __launch_bounds__(64 * (W + LD))
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
               const int row = 16 * u + 8 * h + v_row0;
-              const int piece = (4 * t + v_piece0) ^ swz_v(row);
+              const int piece = (4 * t + v_piece0) ^ swz_v<D>(row);
               h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
                   (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
             }
@@ -805,7 +809,7 @@ __global__ void __launch_bounds__(64 * (2 * T + 2)) __attribute__((amdgpu_waves_
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           const int row = 16 * u + 8 * h + v_row0;
-          const int piece = (4 * t + v_piece0) ^ swz_v(row);
+          const int piece = (4 * t + v_piece0) ^ swz_v<D>(row);
           h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
               (lds_bf16x4*)(Vt + row * TL::ROW_BYTES + piece * 16 + v_sub));
         }
