@@ -158,8 +158,8 @@ def token_position(g: Geometry) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------
-# Blocking (layout transform) and its inverse (§3.3: "rearranged into a
-# blocked layout"; "output blocks are restored to the original layout")
+# Blocking (layout transform) and its inverse (§3.3: Q, K, V enter the
+# blocked layout before attention, and the output returns to raster order)
 # --------------------------------------------------------------------------
 def reorder(X: np.ndarray, g: Geometry) -> np.ndarray:
     """Raster [.., N, d] -> blocked [.., NB*BS, d]; padding slots are zero."""
@@ -191,9 +191,9 @@ def block_means(Xb: np.ndarray, g: Geometry) -> np.ndarray:
 
 # --------------------------------------------------------------------------
 # SICS (§3.2): sum of all pairwise cosine similarities inside one block.
-# Three forms that must agree: Eq. (4) directly; Alg. 1 (online partial sums,
-# from the last line of Eq. (5)); and the squared norm of the sum of unit
-# vectors, which Eq. (5)'s expansion equals term by term.
+# Three forms that must agree: Eq. (4) directly; Eq. (5)'s split into the n
+# self-pairs plus twice the sum over ordered pairs a < b; and the squared norm
+# of the sum of unit vectors, which Eq. (5)'s expansion equals term by term.
 # --------------------------------------------------------------------------
 def _unit_rows(Q: np.ndarray) -> np.ndarray:
     Q = np.asarray(Q, dtype=np.float64)
@@ -213,21 +213,17 @@ def sics_pairwise(Q: np.ndarray) -> float:
     return total
 
 
-def sics_online(Q: np.ndarray) -> float:
-    """Alg. 1: running sum r of unit vectors; sigma += <r, q_j>; return 2 sigma + n.
+def sics_prefix(Q: np.ndarray) -> float:
+    """Eq. (5) split: n + 2 * sum_{a<b} <q^_a, q^_b>, the pair sum taken as each
+    unit row dotted with the exclusive prefix sum of the rows before it.
 
-    The "+ n" counts the diagonal; a zero row has no unit vector, so it adds
-    neither to sigma nor to the diagonal count.
+    A zero row has no unit vector: it adds neither a pair term nor a self term.
     """
     U = _unit_rows(Q)
-    r = np.zeros(U.shape[1])
-    sigma = 0.0
-    diag = 0
-    for j in range(U.shape[0]):
-        sigma += float(r @ U[j])
-        r = r + U[j]
-        diag += int(np.any(U[j] != 0))
-    return 2.0 * sigma + diag
+    before = np.cumsum(U, axis=0) - U          # sum of the unit rows preceding each row
+    pairs = float(np.einsum("jd,jd->", before, U))
+    selfs = int(np.count_nonzero(np.any(U != 0, axis=1)))
+    return selfs + 2.0 * pairs
 
 
 def sics_closed(Q: np.ndarray) -> float:
@@ -238,7 +234,7 @@ def sics_closed(Q: np.ndarray) -> float:
 
 def block_sics(Xb: np.ndarray, g: Geometry, form: str = "closed") -> np.ndarray:
     """[B, H, NB*BS, d] -> [B, H, NB] SICS of each block's valid rows."""
-    fn = {"closed": sics_closed, "online": sics_online, "pairwise": sics_pairwise}[form]
+    fn = {"closed": sics_closed, "prefix": sics_prefix, "pairwise": sics_pairwise}[form]
     _, n_valid = block_tables(g)
     lead = Xb.shape[:-2]
     out = np.empty(lead + (g.NB,), dtype=np.float64)

@@ -1015,13 +1015,10 @@ hipError_t launch_pp(const DevGeom& g, const void* qb, const void* kb, const voi
                      const int* counts, const int* indices, float scale_log2, void* ob,
                      float* lse, hipStream_t s, const MultiTable* tab, const int* order,
                      int nb_max) {
-  static bool attr_set = false;  // the ring and the kept list exceed the 64 KB default
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&attn_pp_kernel<D, T, RASTER, MULTI>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, kPairLds);
+  {  // the ring and the kept list exceed the 64 KB default
+    const hipError_t e = ensure_dynamic_lds(
+        reinterpret_cast<const void*>(&attn_pp_kernel<D, T, RASTER, MULTI>), kPairLds);
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   const size_t lds = size_t(PPLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int);
   const uint4* q4 = static_cast<const uint4*>(qb);
@@ -1044,13 +1041,11 @@ template <int D, int W, bool LD, bool RASTER, bool MULTI>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                      hipStream_t s, const MultiTable* tab = nullptr, const int* order = nullptr) {
-  static bool attr_set = false;  // allow the kept-list LDS beyond the 64 KB default
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(
+  {  // allow the kept-list LDS beyond the 64 KB default
+    const hipError_t e = ensure_dynamic_lds(
         reinterpret_cast<const void*>(&attn_kernel<D, W, LD, RASTER, MULTI>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, int(kMaxAttnNB * sizeof(int)));
+        int(kMaxAttnNB * sizeof(int)));
     if (e != hipSuccess) return e;
-    attr_set = true;
   }
   const uint4* q4 = static_cast<const uint4*>(qb);
   const char* k1 = static_cast<const char*>(kb);

@@ -501,15 +501,10 @@ template <int D, int EST, int SM>
 hipError_t launch_des(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
   const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * 8 +
                      size_t(g.NB) * (4 + 1) + kRows;
-  static bool attr_set = false;  // raising the dynamic-LDS cap once is idempotent
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
-        hipFuncAttributeMaxDynamicSharedMemorySize,
-        int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 8 + kMaxSelectNB * 5 + kRows));
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  const hipError_t e = ensure_dynamic_lds(
+      reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
+      int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 8 + kMaxSelectNB * 5 + kRows));
+  if (e != hipSuccess) return e;
   const dim3 grid((g.NB + kRows - 1) / kRows, g.B * g.H);
   select_kernel<D, EST, SM><<<grid, kThreads, lds, s>>>(g, p);
   return hipGetLastError();

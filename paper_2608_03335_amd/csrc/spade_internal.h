@@ -72,6 +72,11 @@ __device__ __forceinline__ void head_pair(const DevGeom& g, const HeadMap& hm, i
   *raster = int64_t(b) * g.H + (hm.ident ? k : hm.h[k]);
 }
 
+// Raises kernel `fn`'s dynamic-LDS limit to `bytes` on the current device, once per
+// (kernel, device): the attribute is per device, and the first call on each device
+// sets it under a lock (thread-safe; later calls only look it up).
+hipError_t ensure_dynamic_lds(const void* fn, int bytes);
+
 // Launchers (each returns hipGetLastError() after its launches).
 hipError_t launch_reorder(const DevGeom& g, const void* x, void* y, int esize, int inverse,
                           const HeadMap& heads, hipStream_t s);

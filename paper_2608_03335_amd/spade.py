@@ -319,6 +319,16 @@ def spade_compose_select(g: spade_geom, spec: spade_mask_spec, summ: spade_summa
                  stream))
 
 
+def _storage_span(t, elems: int, name: str):
+    """The view t must have `elems` elements of its storage from its first element on."""
+    if not isinstance(t, torch.Tensor):
+        return
+    avail = t.untyped_storage().nbytes() // t.element_size() - t.storage_offset()
+    if elems > avail:
+        raise SpadeError(SPADE_ERR_INVALID_ARG,
+                         f"{name}: the batch strides reach {elems} elements, storage holds {avail}")
+
+
 def spade_sparse_attn_raster_multi(geoms, heads, q, k, v, scale: float, o, lse=None,
                                    workspace=None, stream=None):
     """geoms: sequence of spade_geom; heads: per head (scheme, counts, indices,
@@ -326,11 +336,23 @@ def spade_sparse_attn_raster_multi(geoms, heads, q, k, v, scale: float, o, lse=N
     batch 0 of the head, at least NB and NB*NB elements of its blocking)."""
     a = _Args()
     ga = (spade_geom * len(geoms))(*geoms)
+    heads = list(heads)
+    # the library reads one entry per head of geometry 0: a short table would make it
+    # read past the array (and hand garbage list pointers to the kernel)
+    if len(geoms) and len(heads) != geoms[0].H:
+        raise SpadeError(SPADE_ERR_INVALID_ARG,
+                         f"heads has {len(heads)} entries, geometry 0 has H={geoms[0].H}")
+    B = geoms[0].B if len(geoms) else 0
     rows = []
     for h, (c, cn, ix, cs, xs) in enumerate(heads):
         nb = _Dims(geoms[int(c)]).NB if 0 <= int(c) < len(geoms) else None
         pc = a(cn, I32, nb, f"heads[{h}] counts")
         pi = a(ix, I32, None if nb is None else nb * nb, f"heads[{h}] indices")
+        if nb is not None and B > 1:
+            # batch element b's lists start cs (xs) elements after batch 0's: the whole
+            # span must lie inside the tensor's storage
+            _storage_span(cn, (B - 1) * int(cs) + nb, f"heads[{h}] counts")
+            _storage_span(ix, (B - 1) * int(xs) + nb * nb, f"heads[{h}] indices")
         rows.append(spade_head_lists(int(c), _value(pc), _value(pi), int(cs), int(xs)))
     ha = (spade_head_lists * max(len(rows), 1))(*rows)
     D = _Dims(geoms[0]) if len(geoms) else None

@@ -90,3 +90,57 @@ def sample_rows(B, H, NB, n, seed=0, must=()):
 
 def scale_of(d):
     return 1.0 / math.sqrt(d)
+
+
+def nan_fill(*tensors):
+    """Poison output buffers before a call: a row the kernel skips stays NaN."""
+    for t in tensors:
+        if t is not None and t.is_floating_point():
+            t.fill_(float("nan"))
+
+
+def finite_max_abs(got, ref) -> float:
+    """max |got - ref| over every element, failing on any non-finite GPU value
+    (Python's max() would silently drop a NaN)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    bad = ~np.isfinite(got)
+    assert not bad.any(), f"{int(bad.sum())} non-finite GPU values (first at {np.argwhere(bad)[0].tolist()})"
+    return float(np.max(np.abs(got - ref))) if got.size else 0.0
+
+
+def oracle_attention_on_lists(q, k, v, og, counts, indices, scale, rows=None):
+    """Eq. (2) by the oracle with the given block lists (normally the GPU's own),
+    on fp64 raster q, k, v [B, H, N, d]. Returns (O, lse) in raster order
+    [B, H, N, d] / [B, H, N]; with `rows` only those query blocks are computed."""
+    Qb, Kb, Vb = (O.reorder(x, og) for x in (q, k, v))
+    ob, lb = O.block_sparse_attention(Qb, Kb, Vb, counts, indices, og, scale, rows=rows)
+    pos = O.token_position(og)
+    return ob[:, :, pos], lb[:, :, pos]
+
+
+def row_tokens(og, i) -> np.ndarray:
+    """Raster tokens of query block i's real slots."""
+    slot_token, nv = O.block_tables(og)
+    return slot_token[i * og.BS: i * og.BS + nv[i]]
+
+
+def compare_rows_raster(got_o, got_lse, ref_o, ref_lse, og, rows):
+    """Element-wise attention check of the listed query blocks (b, h, i) on raster
+    outputs; returns the worst max-abs. Every compared value must be finite."""
+    worst = 0.0
+    for (b, h, i) in rows:
+        toks = row_tokens(og, i)
+        worst = max(worst, finite_max_abs(got_o[b, h, toks], ref_o[b, h, toks]))
+        if got_lse is not None:
+            d = finite_max_abs(got_lse[b, h, toks], ref_lse[b, h, toks])
+            assert d <= LSE_MAX_ABS, f"lse of row {(b, h, i)} off by {d:.3e}"
+    return worst
+
+
+def heaviest_head(counts) -> tuple:
+    """(b, h) of the pair holding the row with the most kept blocks (ties: first)."""
+    c = np.asarray(counts)
+    b, h, _ = np.unravel_index(int(np.argmax(c)), c.shape)
+    return int(b), int(h)

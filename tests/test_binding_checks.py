@@ -85,3 +85,26 @@ def test_multi_checks_head_lists():
     call = S.spade_sparse_attn_raster_multi
     _raises(r"heads\[1\] indices", call, [G], [good, short], q, q, q, 0.1, q)
     _raises(r"heads\[0\] counts", call, [G], [wide, good], q, q, q, 0.1, q)
+
+
+def test_multi_checks_table_length_and_batch_spans():
+    q = _raster()
+    good = (0, torch.zeros(NB, dtype=torch.int32), torch.zeros(NB * NB, dtype=torch.int32), 0, 0)
+    call = S.spade_sparse_attn_raster_multi
+    # one entry per head of geometry 0, no fewer and no more
+    _raises("heads has 1 entries", call, [G], [good], q, q, q, 0.1, q)
+    _raises("heads has 3 entries", call, [G], [good] * 3, q, q, q, 0.1, q)
+    # B = 2: batch 1's lists start a stride after batch 0's and must lie in the storage
+    G2 = S.spade_geom(2, 2, 128, 4, 8, 8, 2, 4, 4)
+    q2 = _raster(n=2 * 2 * N * 128)
+    cstore = torch.zeros(2 * NB, dtype=torch.int32)
+    istore = torch.zeros(2 * NB * NB, dtype=torch.int32)
+    ok = (0, cstore[:NB], istore[:NB * NB], NB, NB * NB)
+    far_c = (0, cstore[:NB], istore[:NB * NB], NB + 1, NB * NB)
+    far_i = (0, cstore[:NB], istore[:NB * NB], NB, NB * NB + 1)
+    late = (0, cstore[NB:], istore[NB * NB:], NB, NB * NB)  # batch 0 at the storage's end
+    _raises(r"heads\[0\] counts: the batch strides", call, [G2], [far_c, ok], q2, q2, q2, 0.1, q2)
+    _raises(r"heads\[1\] indices: the batch strides", call, [G2], [ok, far_i], q2, q2, q2, 0.1, q2)
+    _raises(r"heads\[0\] counts: the batch strides", call, [G2], [late, ok], q2, q2, q2, 0.1, q2)
+    # a valid table passes every check up to the device one
+    _raises("GPU tensor", call, [G2], [ok, ok], q2, q2, q2, 0.1, q2)

@@ -144,6 +144,7 @@ def _attention_vs_oracle(cfg, p, Q, K, V, counts, indices, rows=None):
     ci = torch.from_numpy(counts).to(DEV)
     ii = torch.from_numpy(indices).to(DEV)
     p.reorder_in(Q, K, V)
+    P.nan_fill(p.Ob, p.lse)
     p.attend(ci, ii)
     torch.cuda.synchronize()
     Qb, Kb, Vb = (O.reorder(P.to_np64(x), og) for x in (Q, K, V))
@@ -158,11 +159,10 @@ def _attention_vs_oracle(cfg, p, Q, K, V, counts, indices, rows=None):
                                           for i in range(og.NB)]
     for (b, h, i) in todo:
         sl = slice(i * BS, i * BS + nv[i])
-        err = np.max(np.abs(got[b, h, sl] - ref[b, h, sl]))
-        worst = max(worst, err)
+        worst = max(worst, P.finite_max_abs(got[b, h, sl], ref[b, h, sl]))
         assert np.all(got[b, h, i * BS + nv[i]:(i + 1) * BS] == 0), "padding slots must be 0"
         if got_lse is not None:
-            np.testing.assert_allclose(got_lse[b, h, sl], ref_lse[b, h, sl], rtol=0, atol=P.LSE_MAX_ABS)
+            assert P.finite_max_abs(got_lse[b, h, sl], ref_lse[b, h, sl]) <= P.LSE_MAX_ABS
     return worst
 
 
@@ -281,11 +281,16 @@ def test_attention_is_deterministic():
 # ---------------- full attention-layer shapes, bench launch configuration ----------------
 @pytest.mark.parametrize("name,n_rows", [("wan13b", 24), ("hunyuan", 24)])
 def test_full_shape_pipeline(name, n_rows):
+    """The blocked path at the full layer shapes: every row's selection against the
+    oracle; attention (outputs NaN-poisoned before the call) on every query block of
+    the head holding the heaviest row plus sampled blocks of other heads, recomputed by
+    the oracle with the GPU's own lists; every output row finite."""
     cfg = workload(name)
     _say("full", name)
     og = P.geometry(cfg)
     Q, K, V = P.bf16_inputs(cfg)
     p = _path(cfg, with_lse=True)
+    P.nan_fill(p.Ob, p.O, p.lse)
     p.run(Q, K, V)
     torch.cuda.synchronize()
     # selection: oracle on the same bf16 inputs, every row
@@ -293,24 +298,25 @@ def test_full_shape_pipeline(name, n_rows):
     n_ex = P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(),
                                cfg["mode"], cfg.get("tau"))
     _say(f"  selection rows exempt: {n_ex}; block sparsity {O.block_sparsity(c, og.NB):.4f}")
-    # attention: sampled query blocks (incl. first/last) recomputed by the oracle with the
-    # GPU's own lists (identical to the oracle's outside exempt rows)
+    assert bool(torch.isfinite(p.O).all()), "a raster output row was not written"
     cg, ig = p.counts.cpu().numpy(), p.indices.cpu().numpy()
+    hb, hh = P.heaviest_head(cg)
     rows = P.sample_rows(cfg["B"], cfg["H"], og.NB, n_rows, seed=1,
                          must=[(0, 0, 0), (0, cfg["H"] - 1, og.NB - 1)])
+    rows = sorted(set(rows) | {(hb, hh, r) for r in range(og.NB)})
     Qb, Kb, Vb = (O.reorder(P.to_np64(x), og) for x in (Q, K, V))
-    # restrict the blocked copies to sampled heads to bound host memory
     ref, ref_lse = O.block_sparse_attention(Qb, Kb, Vb, cg, ig, og, P.scale_of(cfg["d"]), rows=rows)
     got = P.to_np64(p.Ob)
+    got_lse = p.lse.cpu().numpy().astype(np.float64)
     O_raster = P.to_np64(p.O)
     pos = O.token_position(og)
     _, nv = O.block_tables(og)
     worst = 0.0
     for (b, h, i) in rows:
         sl = slice(i * og.BS, i * og.BS + nv[i])
-        worst = max(worst, float(np.max(np.abs(got[b, h, sl] - ref[b, h, sl]))))
-        np.testing.assert_allclose(p.lse.cpu().numpy()[b, h, sl], ref_lse[b, h, sl], atol=P.LSE_MAX_ABS, rtol=0)
+        worst = max(worst, P.finite_max_abs(got[b, h, sl], ref[b, h, sl]))
+        assert P.finite_max_abs(got_lse[b, h, sl], ref_lse[b, h, sl]) <= P.LSE_MAX_ABS
     # restore layer: the raster output is the inverse permutation of the blocked one
     assert np.array_equal(O_raster, got[:, :, pos])
-    _say(f"  attention max-abs over {len(rows)} sampled query blocks: {worst:.3e}")
+    _say(f"  attention max-abs over {len(rows)} query blocks (head {hh} whole): {worst:.3e}")
     assert worst <= P.ATTN_MAX_ABS

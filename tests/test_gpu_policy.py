@@ -65,6 +65,7 @@ def test_policy_sweep_matches_oracle(func):
     Q, K, V = P.bf16_inputs(cfg)
     pol = Policy(func)
     p = SweepPath(1, 6, 64, *grid, cands, 0.7, device=DEV, policy=pol)
+    P.nan_fill(p.O)
     p.evaluate(Q, K)
     work = p.work_list(torch.cuda.current_stream())
     best = p.best.cpu().numpy()
@@ -95,8 +96,10 @@ def test_policy_sweep_matches_oracle(func):
             sl = (slice(None), slice(k, k + 1))
             n_ex += P.compare_selection(ref["scores"][sl], ref["inter_counts"][sl],
                                         ref["inter_indices"][sl], cv[sl], iv[sl], "topk")
-        ref_O[:, heads] = ref["O"]
-    if n_ex == 0:
-        err = float(np.max(np.abs(P.to_np64(p.O) - ref_O)))
-        _say(f"  max-abs {err:.3e}")
-        assert err <= P.ATTN_MAX_ABS
+        # attention of the group on the GPU's own lists, every element
+        ro, _ = P.oracle_attention_on_lists(Qn[:, heads], Kn[:, heads], Vn[:, heads], og, c_g, i_g,
+                                            scale)
+        ref_O[:, heads] = ro
+    err = P.finite_max_abs(P.to_np64(p.O), ref_O)
+    _say(f"  exempt rows {n_ex}, max-abs {err:.3e}")
+    assert err <= P.ATTN_MAX_ABS

@@ -166,14 +166,17 @@ def test_sweep_small_smooth_fields(sparsity):
     _say("sweep smooth", sparsity)
     Q, K, V = P.bf16_inputs(cfg)
     p = _sweep_path(cfg, cands, sparsity)
+    P.nan_fill(p.O)
     p.run(Q, K, V)
     torch.cuda.synchronize()
     q, k, v = (P.to_np64(x) for x in (Q, K, V))
     ref = O.spade_sweep_attention(q, k, v, grid, cands, sparsity)
-    ch_ref = _check_choice(p.as_qk.cpu().numpy(), ref["as_qk"], p.choice.cpu().numpy())
-    if not np.array_equal(p.choice.cpu().numpy(), ch_ref):
-        pytest.skip("near-tie between candidates; outputs not comparable")
-    worst = 0.0
+    # the GPU's choice must be the oracle's, or one of a near-tie (checked here)
+    _check_choice(p.as_qk.cpu().numpy(), ref["as_qk"], p.choice.cpu().numpy())
+    # every group, under the GPU's own choice: selection against the oracle's, and the
+    # attention against the oracle run on the GPU's lists, every element, every run
+    ref_O = np.full(q.shape, np.nan)
+    n_ex = 0
     for c, heads in p.work_list():
         g = O.Geometry(*grid, *cands[c])
         v_ = p.group_views(c, len(heads))
@@ -181,11 +184,13 @@ def test_sweep_small_smooth_fields(sparsity):
         kbar = O.block_means(O.reorder(k[:, heads], g), g)
         s = O.block_scores(qbar, kbar, P.scale_of(128))
         c_o, i_o = O.select(s, "topk", topk=O.sweep_topk(sparsity, g.NB))
-        n_ex = P.compare_selection(s, c_o, i_o, v_["counts"].cpu().numpy(),
-                                   v_["indices"].cpu().numpy(), "topk")
-        if n_ex == 0:
-            worst = max(worst, float(np.max(np.abs(P.to_np64(p.O)[:, heads] - ref["O"][:, heads]))))
-    _say(f"  groups {p.work_list()} max-abs {worst:.3e}")
+        cg, ig = v_["counts"].cpu().numpy(), v_["indices"].cpu().numpy()
+        n_ex += P.compare_selection(s, c_o, i_o, cg, ig, "topk")
+        ro, _ = P.oracle_attention_on_lists(q[:, heads], k[:, heads], v[:, heads], g, cg, ig,
+                                            P.scale_of(128))
+        ref_O[:, heads] = ro
+    worst = P.finite_max_abs(P.to_np64(p.O), ref_O)
+    _say(f"  groups {p.work_list()} exempt rows {n_ex} max-abs {worst:.3e}")
     assert worst <= P.ATTN_MAX_ABS
 
 
@@ -199,8 +204,10 @@ def test_sweep_full_hunyuan_shape():
     _say("sweep full hunyuan")
     Q, K, V = P.bf16_inputs(cfg)
     p = _sweep_path(cfg, cands, sparsity)
+    P.nan_fill(p.O)
     p.run(Q, K, V)
     torch.cuda.synchronize()
+    assert bool(torch.isfinite(p.O).all()), "an output row was not written"
     heads = list(range(0, cfg["H"], 4))          # every 4th head: all four field types
     q, k = (P.to_np64(x[:, heads]) for x in (Q, K))
     grid = (cfg["T"], cfg["Hs"], cfg["Ws"])
@@ -231,7 +238,7 @@ def test_sweep_full_hunyuan_shape():
         pos = O.token_position(g)
         for (b, h, i) in rows:
             sl = slice(i * g.BS, i * g.BS + nv[i])
-            worst = max(worst, float(np.max(np.abs(got[b, h, sl] - ref[b, h, sl]))))
+            worst = max(worst, P.finite_max_abs(got[b, h, sl], ref[b, h, sl]))
         # the group's blocked output went to its own heads of the raster output
         for j, jj in enumerate(sample):
             assert np.array_equal(out[:, grp[jj]], got[:, j][:, pos])

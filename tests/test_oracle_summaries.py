@@ -40,7 +40,7 @@ def _rand_block(rng, n, d):
 @pytest.mark.parametrize("n,d", [(1, 4), (2, 3), (7, 16), (32, 64), (45, 8)])
 def test_three_sics_forms_agree(n, d):
     Q = _rand_block(np.random.default_rng(n * 100 + d), n, d)
-    a, b, c = O.sics_pairwise(Q), O.sics_online(Q), O.sics_closed(Q)
+    a, b, c = O.sics_pairwise(Q), O.sics_prefix(Q), O.sics_closed(Q)
     assert abs(a - c) <= 1e-9 * max(1.0, abs(a))
     assert abs(b - c) <= 1e-9 * max(1.0, abs(a))
     assert -1e-12 <= c <= n * n + 1e-9
@@ -52,10 +52,10 @@ def test_sics_special_cases():
     par = np.outer(rng.uniform(0.5, 2.0, 10), v)          # parallel rows -> n^2
     assert math.isclose(O.sics_closed(par), 100.0, rel_tol=1e-12)
     pm = np.stack([v, -2 * v, 3 * v, -0.5 * v])             # +/- pairs cancel -> 0
-    assert abs(O.sics_closed(pm)) < 1e-12 and abs(O.sics_online(pm)) < 1e-12
+    assert abs(O.sics_closed(pm)) < 1e-12 and abs(O.sics_prefix(pm)) < 1e-12
     orth = np.linalg.qr(rng.standard_normal((8, 8)))[0][:5] * rng.uniform(0.1, 9, (5, 1))
     assert math.isclose(O.sics_pairwise(orth), 5.0, rel_tol=1e-12)  # orthogonal -> n
-    assert math.isclose(O.sics_online(orth), 5.0, rel_tol=1e-12)
+    assert math.isclose(O.sics_prefix(orth), 5.0, rel_tol=1e-12)
 
 
 def test_sics_is_invariant_to_positive_row_scaling():
