@@ -359,6 +359,25 @@ spade_status spade_sparse_attn_raster(const spade_geom* g, const void* q, const 
                                       void* workspace, size_t workspace_bytes,
                                       hipStream_t stream);
 
+/*
+ * spade_sparse_attn_raster without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc). Arguments, results and errors are those of
+ * spade_sparse_attn_raster, bit for bit; the schedule's scratch (the head ranking,
+ * 16 bytes per (batch, head) pair) lives in a 64 KiB array the library holds in
+ * each GPU's memory until the process ends, so the call allocates nothing. Its
+ * address is looked up once per device, on the first call there (a failed lookup
+ * returns SPADE_ERR_HIP). The ranking rewrites every scratch byte it reads, so no
+ * clearing is needed; a problem whose schedule needs more scratch than the array
+ * holds returns SPADE_ERR_UNSUPPORTED (with at most 4096 pairs none does).
+ * All calls on one GPU share the array: calls that may overlap on that GPU (other
+ * streams, other threads) race and must be ordered by the caller.
+ */
+spade_status spade_sparse_attn_raster_noalloc(const spade_geom* g, const void* q, const void* k,
+                                              const void* v, const int32_t* counts,
+                                              const int32_t* indices, double scale, void* o,
+                                              float* lse, hipStream_t stream);
+
 /* Block lists of one head for spade_sparse_attn_raster_multi (device pointers). */
 typedef struct {
   int32_t scheme;           /* index of the head's blocking among the call's geometries */

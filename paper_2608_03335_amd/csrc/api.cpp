@@ -494,4 +494,25 @@ spade_status spade_sparse_attn_raster(const spade_geom* g, const void* q, const 
                      stream);
 }
 
+spade_status spade_sparse_attn_raster_noalloc(const spade_geom* g, const void* q, const void* k,
+                                              const void* v, const int32_t* counts,
+                                              const int32_t* indices, double scale, void* o,
+                                              float* lse, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  const size_t need = empty ? 0 : spade::attn_workspace_bytes(dg);
+  if (need > spade::kNoAllocScratchBytes)
+    return fail(SPADE_ERR_UNSUPPORTED, "the schedule needs %zu bytes of scratch, the library holds %zu",
+                need, spade::kNoAllocScratchBytes);
+  void* ws = nullptr;
+  size_t ws_bytes = 0;
+  if (need > 0) {
+    const hipError_t e = spade::noalloc_scratch(&ws, &ws_bytes);
+    if (e != hipSuccess) return hip_status(e, "scratch lookup");
+  }
+  return sparse_attn(g, q, k, v, counts, indices, scale, o, lse, ws, ws_bytes, true, stream);
+}
+
 }  // extern "C"

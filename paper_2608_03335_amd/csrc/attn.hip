@@ -38,9 +38,17 @@
 // chunks skip the 64-register rescale; row sums use bf16 dot2 on the same packed
 // P that feeds the MFMA.
 #include <climits>
+#include <mutex>
 #include <type_traits>
 
 #include "spade_internal.h"
+
+// Scratch of the allocation-free raster attention call: the head ranking's keys
+// and order, 16 bytes per (batch, head) pair for at most spade::kMaxRankedHeads
+// pairs (beyond that the launch runs in grid order and needs none). Each GPU holds
+// its own copy until the process ends; host code reaches it only through the
+// address hipGetSymbolAddress returns on that device.
+static __device__ __align__(256) unsigned char scratch[spade::kNoAllocScratchBytes];
 
 namespace spade {
 namespace {
@@ -1101,7 +1109,6 @@ hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void
 // ties to the lower index), so long rows start first instead of forming the
 // tail; within a head each XCD takes its rows heaviest first (heavy_first).
 constexpr int kRankThreads = 1024;
-constexpr int kMaxRankedHeads = 4096;  // beyond this many (batch, head) pairs: grid order
 
 __global__ void __launch_bounds__(256) head_keys_kernel(DevGeom g, const int* __restrict__ counts,
                                                         uint64_t* __restrict__ keys) {
@@ -1209,6 +1216,25 @@ size_t ranked_pairs(const DevGeom& g) {
 }
 
 }  // namespace
+
+hipError_t noalloc_scratch(void** ptr, size_t* bytes) {
+  static std::mutex mu;
+  static void* by_device[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (by_device[dev] == nullptr) {  // first call on this device: look the copy up once
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    by_device[dev] = p;
+  }
+  *ptr = by_device[dev];
+  *bytes = kNoAllocScratchBytes;
+  return hipSuccess;
+}
 
 size_t attn_workspace_bytes(const DevGeom& g) {
   // keys (8 B) of every pair, then the order (4 B; a multi-scheme launch also

@@ -148,6 +148,12 @@ hipError_t launch_block_sparse_attn(const DevGeom& g, const void* qb, const void
                                     float scale, void* ob, float* lse, void* ws, bool raster,
                                     hipStream_t s);
 
+constexpr int kMaxRankedHeads = 4096;  // attention head ranking; beyond: grid order
+// scratch of the allocation-free attention call: the ranking of kMaxRankedHeads pairs
+constexpr size_t kNoAllocScratchBytes = size_t(kMaxRankedHeads) * 16;
+constexpr int kMaxDevices = 64;
+// This device's copy of that scratch (looked up once per device, thread-safe).
+hipError_t noalloc_scratch(void** ptr, size_t* bytes);
 constexpr int kMaxBS = 256;        // attention: one wave per 32 query rows, <= 8 waves
 constexpr int kMaxSelectNB = 1024;  // selection: one row of scores per wave in registers
 constexpr int kMaxAttnNB = 16384;   // attention: a work item's kept list is staged in LDS

@@ -31,7 +31,8 @@ EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
             "spade_compose_select", "spade_policy_budgets", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_sparse_attn_raster",
-            "spade_sparse_attn_raster_multi", "spade_status_string",
+            "spade_sparse_attn_raster_multi", "spade_sparse_attn_raster_noalloc",
+            "spade_status_string",
             "spade_last_error")
 MAX_HEAD_LIST = 64
 
@@ -111,6 +112,7 @@ def lib() -> ctypes.CDLL:
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
+            "spade_sparse_attn_raster_noalloc": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp]),
             "spade_sparse_attn_raster_multi": (i32, [G, i32, ctypes.POINTER(spade_head_lists), vp,
                                                      vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_status_string": (ctypes.c_char_p, [i32]),
@@ -401,3 +403,15 @@ def spade_sparse_attn_raster(g: spade_geom, q, k, v, counts, indices, scale: flo
                  a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
                  float(scale), a(o, BF16, D.raster, "o"), a(lse, F32, D.raster_rows, "lse"),
                  a(workspace, None, None, "workspace"), nbytes, stream))
+
+
+def spade_sparse_attn_raster_noalloc(g: spade_geom, q, k, v, counts, indices, scale: float, o,
+                                     lse=None, stream=None):
+    """spade_sparse_attn_raster with the library's own per-GPU scratch (no workspace)."""
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_sparse_attn_raster_noalloc, ctypes.byref(g),
+                 a(q, BF16, D.raster, "q"), a(k, BF16, D.raster, "k"), a(v, BF16, D.raster, "v"),
+                 a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
+                 float(scale), a(o, BF16, D.raster, "o"), a(lse, F32, D.raster_rows, "lse"),
+                 stream))
