@@ -74,7 +74,11 @@ policy study), which the paper describes by its effect only:
   * AS-guided budgets: head h gets k_h = clamp(floor(H k_dyn w_h / W + 1/2), 1, NB)
     with w_h = 1 / AS_h (budget negatively correlated with the Selected
     Aggregation Score; w_h = 0 when AS_h <= 0) and W the sum of the w_h in head
-    order (W = 0: every head gets clamp(k_dyn, 1, NB)).
+    order (W = 0: every head gets clamp(k_dyn, 1, NB));
+  * for Top-P schemes the budget is the mass: head h keeps tau_h = 1 - e_h with
+    the dropped mass e_h = H (1 - tau) AS_h / S proportional to its score (S the
+    sum of the positive scores in head order; AS_h <= 0 drops nothing; S = 0:
+    tau for every head), so the mean dropped mass stays 1 - tau.
 
 Every array here is float64 (inputs are upcast first). Shapes: Q, K, V are
 [B, H, N, d]; blocked tensors are [B, H, NB*BS, d].
@@ -683,6 +687,24 @@ def policy_head_budgets(as_best, k_dyn: int, NB: int) -> np.ndarray:
     total = float(H) * float(k_dyn)
     return np.array([min(max(int(np.floor(total * x / W + 0.5)), 1), NB) for x in w],
                     dtype=np.int32)
+
+
+def policy_head_tau(as_best, tau: float) -> np.ndarray:
+    """Per-head Top-P mass for a Top-P scheme, negatively correlated with the
+    Selected AS (reading): the dropped mass 1 - tau is spread over the heads in
+    proportion to their score, e_h = (H (1 - tau)) * AS_h / S with S the sum of the
+    positive scores in head order, and tau_h = 1 - e_h. The mean dropped mass stays
+    1 - tau; a head with AS <= 0 drops nothing (tau_h = 1); S = 0 gives every head
+    tau. tau_h may fall to or below 0, which keeps only the top block."""
+    a = [max(float(x), 0.0) for x in as_best]
+    H = len(a)
+    S = 0.0
+    for x in a:                      # head order, one addition at a time
+        S += x
+    if not S > 0.0:
+        return np.full(H, float(tau))
+    total = float(H) * (1.0 - float(tau))
+    return np.array([1.0 - total * x / S for x in a], dtype=np.float64)
 
 
 # --------------------------------------------------------------------------

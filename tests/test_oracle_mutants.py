@@ -219,3 +219,12 @@ def test_warmup_rounded_down_is_caught(monkeypatch):
         return step < int(np.floor((0.30 if task == "t2v" else 0.25) * n))
     monkeypatch.setattr(O, "policy_dense", floor_warmup)
     assert _fails(TP.test_dense_warmup_steps, 50, "i2v", False, 12)
+
+
+def test_tau_positively_correlated_with_the_score_is_caught(monkeypatch):
+    orig = O.policy_head_tau
+
+    def inverse(as_best, tau):  # spreads the dropped mass by 1 / AS instead of AS
+        return orig([1.0 / a if a > 0 else 0.0 for a in as_best], tau)
+    monkeypatch.setattr(O, "policy_head_tau", inverse)
+    assert _fails(TP.test_head_tau_falls_as_scores_rise_and_keeps_the_mean)

@@ -66,3 +66,28 @@ def test_budgets_clamp_and_degenerate_scores():
     assert k.tolist() == [360, 1]
     assert O.policy_head_budgets([0.0, -1.0, 2.0], 10, 100).tolist() == [1, 1, 30]
     assert O.policy_head_budgets([0.0, 0.0], 7, 5).tolist() == [5, 5]
+
+
+def test_head_tau_by_hand():
+    # dropped mass 4 x 0.1 = 0.4 spread as AS / 4: (0.1, 0.15, 0.05, 0.1)
+    got = O.policy_head_tau([1.0, 1.5, 0.5, 1.0], 0.9)
+    assert np.allclose(got, [0.9, 0.85, 0.95, 0.9], rtol=0, atol=1e-15)
+    # a head without a positive score drops nothing; the others share 3 x 0.2
+    got = O.policy_head_tau([0.0, 2.0, 1.0], 0.8)
+    assert np.allclose(got, [1.0, 0.6, 0.8], rtol=0, atol=1e-15)
+    # no score at all: the flat tau; a dominant head can fall below 0 (top block only)
+    assert O.policy_head_tau([0.0, -3.0], 0.7).tolist() == [0.7, 0.7]
+    assert O.policy_head_tau([10.0, 0.001], 0.3)[0] < 0.0
+
+
+def test_head_tau_falls_as_scores_rise_and_keeps_the_mean():
+    rng = np.random.default_rng(2)
+    for H, tau in ((24, 0.9), (40, 0.95), (12, 0.8)):
+        a = rng.uniform(0.4, 1.9, H)
+        t = O.policy_head_tau(a, tau)
+        order = np.argsort(a, kind="stable")
+        assert np.all(np.diff(t[order]) <= 0)
+        assert abs(float(np.mean(1.0 - t)) - (1.0 - tau)) <= 1e-12
+        assert np.array_equal(t, O.policy_head_tau(a * 3.0, tau)) or \
+            np.allclose(t, O.policy_head_tau(a * 3.0, tau), rtol=0, atol=1e-15)
+    assert np.all(O.policy_head_tau([0.6] * 24, 0.9) == 0.9)
