@@ -17,6 +17,9 @@
  *                            intra-block filter, local window and attention sink
  *   spade_policy_budgets     per-head dynamic budgets from the Selected
  *                            Aggregation Score (the policy function, §3.1)
+ *   spade_policy_tau         the same for Top-P schemes (per-head mass)
+ *   spade_policy_dense       the policy's dense warm-up schedule (host)
+ *   spade_policy_split       the policy's static/dynamic budget split (host)
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  *   spade_sparse_attn_raster_multi  the same over heads with different blockings
@@ -300,6 +303,56 @@ spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* sp
 spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_t* heads,
                                   int32_t n_heads, int32_t k_dyn, int32_t NB, int32_t* k_out,
                                   hipStream_t stream);
+
+/*
+ * Head-wise Top-P mass of the policy function — paper §3.1 and §4 (as for
+ * spade_policy_budgets) for a Top-P scheme. The output feeds
+ * spade_mask_spec.tau_per_head.
+ *
+ *   as_best, H, heads, n_heads: as for spade_policy_budgets.
+ *   tau:     the scheme's mass, in (0, 1].
+ *   tau_out: out, fp64 [n] device, in list order: tau_k = 1 - n (1 - tau) a_k / S with
+ *            a_k = max(AS of the head, 0) and S the sum of the listed heads' a in list
+ *            order (S = 0: every head gets tau). The dropped mass is spread over the
+ *            heads in proportion to their score, so it averages 1 - tau; a value
+ *            <= 0 keeps only each row's top block. fp64, correctly rounded
+ *            operations in a fixed order: deterministic.
+ *   H == 0 or an empty list is a no-op.
+ */
+spade_status spade_policy_tau(const double* as_best, int32_t H, const int32_t* heads,
+                              int32_t n_heads, double tau, double* tau_out, hipStream_t stream);
+
+enum { SPADE_TASK_T2V = 0, SPADE_TASK_I2V = 1 };  /* denoising task of spade_policy_dense */
+
+/*
+ * Warm-up schedule of the policy function — paper §4.1 (configurations): full
+ * attention for the first 30% of the denoising steps in text-to-video and 25% in
+ * image-to-video; SPADE-Turbo only for the first step. Host function (no GPU).
+ *
+ *   step:   0-based denoising step, 0 <= step < n_steps.
+ *   task:   SPADE_TASK_T2V or SPADE_TASK_I2V; turbo: nonzero for SPADE-Turbo.
+ *   dense:  out (host): 1 when the step runs full attention: step < ceil(0.3 n_steps)
+ *           (t2v) or step < ceil(0.25 n_steps) (i2v); Turbo: step < 1. Else 0.
+ */
+spade_status spade_policy_dense(int32_t step, int32_t n_steps, int32_t task, int32_t turbo,
+                                int32_t* dense);
+
+/*
+ * Static/dynamic budget split of a head-wise scheme — paper §4.1: Func 0 gives
+ * the dynamic and static parts a 30:1 budget, Func 1 about 80% dynamic. Host
+ * function (no GPU).
+ *
+ *   k_total: blocks per row (>= 1); func: 0 or 1.
+ *   The static share, round(k_total / 31) (Func 0) or round(k_total / 5) (Func 1),
+ *   halves rounded up, buys the largest window of the radius ladder
+ *   (t, y, x) = (0,0,0), (0,0,1), (0,1,1), (1,1,1), (1,1,2), (1,2,2), (2,2,2)
+ *   (1, 3, 9, 27, 45, 75, 125 blocks) that fits; the dynamic Top-K keeps the rest.
+ *   window:  out (host) int32 [3]: the radii, or -1, -1, -1 when no window fits.
+ *   window_blocks: out (host): the window's block count (0 without a window).
+ *   k_dyn:   out (host): k_total - window_blocks.
+ */
+spade_status spade_policy_split(int32_t k_total, int32_t func, int32_t* window,
+                                int32_t* window_blocks, int32_t* k_dyn);
 
 /*
  * Scratch bytes spade_block_sparse_attn and spade_sparse_attn_raster need for

@@ -390,6 +390,53 @@ spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_
                     "policy_budgets launch");
 }
 
+spade_status spade_policy_tau(const double* as_best, int32_t H, const int32_t* heads,
+                              int32_t n_heads, double tau, double* tau_out, hipStream_t stream) {
+  if (H < 0 || H > 65535) return fail(SPADE_ERR_INVALID_ARG, "H must lie in [0, 65535] (got %d)", H);
+  if (!(tau > 0.0 && tau <= 1.0))
+    return fail(SPADE_ERR_INVALID_ARG, "tau must lie in (0, 1] (got %g)", tau);
+  spade::DevGeom dg = {};
+  dg.H = H;
+  spade::HeadMap hm;
+  spade_status st = parse_heads(dg, heads, n_heads, &hm);
+  if (st != SPADE_OK) return st;
+  if (hm.n == 0) return SPADE_OK;
+  if (!as_best || !tau_out)
+    return fail(SPADE_ERR_INVALID_ARG, "as_best and tau_out must be non-null");
+  return hip_status(spade::launch_policy_tau(as_best, hm, tau, tau_out, stream),
+                    "policy_tau launch");
+}
+
+spade_status spade_policy_dense(int32_t step, int32_t n_steps, int32_t task, int32_t turbo,
+                                int32_t* dense) {
+  if (!dense) return fail(SPADE_ERR_INVALID_ARG, "dense must be non-null");
+  if (n_steps < 1) return fail(SPADE_ERR_INVALID_ARG, "n_steps must be >= 1 (got %d)", n_steps);
+  if (step < 0 || step >= n_steps)
+    return fail(SPADE_ERR_INVALID_ARG, "step must lie in [0, n_steps) (got %d of %d)", step,
+                n_steps);
+  if (n_steps > (1 << 27)) return fail(SPADE_ERR_UNSUPPORTED, "n_steps above 2^27");
+  if (task != SPADE_TASK_T2V && task != SPADE_TASK_I2V)
+    return fail(SPADE_ERR_INVALID_ARG, "task must be SPADE_TASK_T2V or SPADE_TASK_I2V (got %d)",
+                task);
+  *dense = spade::policy_dense(step, n_steps, task, turbo != 0) ? 1 : 0;
+  return SPADE_OK;
+}
+
+spade_status spade_policy_split(int32_t k_total, int32_t func, int32_t* window,
+                                int32_t* window_blocks, int32_t* k_dyn) {
+  if (!window || !window_blocks || !k_dyn)
+    return fail(SPADE_ERR_INVALID_ARG, "window, window_blocks and k_dyn must be non-null");
+  if (k_total < 1 || k_total > (1 << 27))
+    return fail(SPADE_ERR_INVALID_ARG, "k_total must lie in [1, 2^27] (got %d)", k_total);
+  if (func != 0 && func != 1) return fail(SPADE_ERR_INVALID_ARG, "func must be 0 or 1 (got %d)", func);
+  int w[3], wb = 0, kd = 0;
+  spade::policy_split(k_total, func, w, &wb, &kd);
+  for (int a = 0; a < 3; ++a) window[a] = w[a];
+  *window_blocks = wb;
+  *k_dyn = kd;
+  return SPADE_OK;
+}
+
 spade_status spade_compose_select(const spade_geom* g, const spade_mask_spec* spec,
                                   const spade_summaries* sum, int32_t* counts, int32_t* indices,
                                   double* scores, hipStream_t stream) {

@@ -116,6 +116,10 @@ struct SelectSpec {
   double* scores;
 };
 hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
+hipError_t launch_policy_tau(const double* as_best, const HeadMap& hm, double tau,
+                             double* tau_out, hipStream_t s);
+bool policy_dense(int step, int n_steps, int task, bool turbo);
+void policy_split(int k_total, int func, int window[3], int* window_blocks, int* k_dyn);
 hipError_t launch_policy_budgets(const double* as_best, const HeadMap& hm, int k_dyn, int NB,
                                  int* k_out, hipStream_t s);
 size_t attn_workspace_bytes(const DevGeom& g);

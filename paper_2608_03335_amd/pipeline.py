@@ -203,12 +203,16 @@ class SweepPath:
     """
 
     def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda",
-                 policy=None, raster=False):
+                 policy=None, raster=False, tau=None):
         self.B, self.H, self.d = B, H, d
         self.raster = bool(raster)
         if self.raster and H > S.MAX_HEAD_LIST:
             raise ValueError(f"raster sweep supports at most {S.MAX_HEAD_LIST} heads")
         self.policy = policy  # None: uniform k per group; else the policy function's budgets
+        # row rule of the groups: Top-K with k = max(1, round((1 - s) NB)) (tau None), or
+        # Top-P with mass tau (the policy then spreads the mass over the heads, and the
+        # Top-K budget only sizes its static window)
+        self.tau = None if tau is None else float(tau)
         self.shapes = [tuple(c) for c in candidates]
         self.sparsity = float(sparsity)
         self.scale = float(scale if scale is not None else 1.0 / math.sqrt(d))
@@ -238,7 +242,8 @@ class SweepPath:
                 kbar=torch.empty(B * cap * g.NB * d, dtype=f64, device=dev),
                 counts=torch.empty(B * cap * g.NB, dtype=torch.int32, device=dev),
                 indices=torch.empty(B * cap * g.NB * g.NB, dtype=torch.int32, device=dev),
-                k_heads=torch.empty(cap, dtype=torch.int32, device=dev)))
+                k_heads=torch.empty(cap, dtype=torch.int32, device=dev),
+                tau_heads=torch.empty(cap, dtype=f64, device=dev)))
         self.ws = torch.empty(max(max(S.spade_attn_workspace_bytes(g) for g in self.geoms), 1),
                               dtype=torch.uint8, device=dev)
         self.O = torch.empty((B, H, T * Hs * Ws, d), dtype=bf, device=dev)
@@ -281,15 +286,25 @@ class SweepPath:
                                     stream=stream)
             S.spade_block_reorder(g, V, v["V"], heads=heads, stream=stream)
         if self.policy is None:
-            S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], S.SPADE_TOPK, self.topk[c], 1.0,
-                                    self.scale, v["counts"], v["indices"], stream=stream)
+            mode = S.SPADE_TOPK if self.tau is None else S.SPADE_TOPP
+            S.spade_estimate_select(v["g"], v["qbar"], v["kbar"], mode, self.topk[c],
+                                    1.0 if self.tau is None else self.tau, self.scale,
+                                    v["counts"], v["indices"], stream=stream)
             return v
-        # the policy function: static window + per-head k from the Selected AS (§3.1)
-        kh = self.gb[c]["k_heads"][: len(heads)]
-        sc = self.policy.scheme(self.topk[c], g.NB, self.best, kh, heads=heads, stream=stream)
+        if self.tau is None:
+            # the policy function: static window + per-head k from the Selected AS (§3.1)
+            kh = self.gb[c]["k_heads"][: len(heads)]
+            sc = self.policy.scheme(self.topk[c], g.NB, self.best, kh, heads=heads, stream=stream)
+            spec = S.mask_spec(S.SPADE_EST_MEAN, S.SPADE_TOPK, sc.topk, 1.0, self.scale, kh, None,
+                               S.SPADE_INTRA_NONE, 0, 0.0, sc.window, 0)
+        else:
+            # Top-P: the same window, and per-head mass from the Selected AS
+            th = self.gb[c]["tau_heads"][: len(heads)]
+            sc = self.policy.scheme_topp(self.tau, self.topk[c], self.best, th, heads=heads,
+                                         stream=stream)
+            spec = S.mask_spec(S.SPADE_EST_MEAN, S.SPADE_TOPP, 1, self.tau, self.scale, None, th,
+                               S.SPADE_INTRA_NONE, 0, 0.0, sc.window, 0)
         v["scheme"] = sc
-        spec = S.mask_spec(S.SPADE_EST_MEAN, S.SPADE_TOPK, sc.topk, 1.0, self.scale, kh, None,
-                           S.SPADE_INTRA_NONE, 0, 0.0, sc.window, 0)
         S.spade_compose_select(v["g"], spec, S.summaries(v["qbar"], v["kbar"]), v["counts"],
                                v["indices"], stream=stream)
         return v

@@ -25,11 +25,13 @@ SPADE_BF16, SPADE_FP32 = 0, 1
 SPADE_TOPK, SPADE_TOPP = 0, 1
 SPADE_EST_MEAN, SPADE_EST_DSA, SPADE_EST_DSA2 = 0, 1, 2
 SPADE_INTRA_NONE, SPADE_INTRA_THRESHOLD, SPADE_INTRA_TOPK = 0, 1, 2
+SPADE_TASK_T2V, SPADE_TASK_I2V = 0, 1
 
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
-            "spade_compose_select", "spade_policy_budgets", "spade_attn_workspace_bytes",
+            "spade_compose_select", "spade_policy_budgets", "spade_policy_tau",
+            "spade_policy_dense", "spade_policy_split", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_sparse_attn_raster",
             "spade_sparse_attn_raster_multi", "spade_sparse_attn_raster_noalloc",
             "spade_status_string",
@@ -109,6 +111,10 @@ def lib() -> ctypes.CDLL:
             "spade_compose_select": (i32, [G, ctypes.POINTER(spade_mask_spec),
                                            ctypes.POINTER(spade_summaries), vp, vp, vp, vp]),
             "spade_policy_budgets": (i32, [vp, i32, ctypes.POINTER(i32), i32, i32, i32, vp, vp]),
+            "spade_policy_tau": (i32, [vp, i32, ctypes.POINTER(i32), i32, f64, vp, vp]),
+            "spade_policy_dense": (i32, [i32, i32, i32, i32, ctypes.POINTER(i32)]),
+            "spade_policy_split": (i32, [i32, i32, ctypes.POINTER(i32), ctypes.POINTER(i32),
+                                         ctypes.POINTER(i32)]),
             "spade_attn_workspace_bytes": (sz, [G]),
             "spade_block_sparse_attn": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
             "spade_sparse_attn_raster": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp, sz, vp]),
@@ -375,6 +381,34 @@ def spade_policy_budgets(as_best, k_dyn: int, NB: int, k_out, heads=None, stream
     _check(a.run(lib().spade_policy_budgets, a(as_best, F64, None, "as_best"), H, arr, n,
                  int(k_dyn), int(NB), a(k_out, I32, n if heads is not None else H, "k_out"),
                  stream))
+
+
+def spade_policy_tau(as_best, tau: float, tau_out, heads=None, stream=None):
+    """as_best: fp64 [H] device tensor; tau_out: fp64 [len(heads) or H] device tensor."""
+    a = _Args()
+    arr, n = _head_list(heads)
+    H = int(as_best.numel())
+    _check(a.run(lib().spade_policy_tau, a(as_best, F64, None, "as_best"), H, arr, n, float(tau),
+                 a(tau_out, F64, n if heads is not None else H, "tau_out"), stream))
+
+
+def spade_policy_dense(step: int, n_steps: int, task: int = SPADE_TASK_T2V,
+                       turbo: bool = False) -> bool:
+    """Host call: does denoising step `step` of n_steps run full attention?"""
+    out = ctypes.c_int32(0)
+    _check(lib().spade_policy_dense(int(step), int(n_steps), int(task), int(bool(turbo)),
+                                    ctypes.byref(out)))
+    return bool(out.value)
+
+
+def spade_policy_split(k_total: int, func: int):
+    """Host call: (window radii or None, window blocks, dynamic k) for k_total blocks."""
+    w = (ctypes.c_int32 * 3)()
+    wb, kd = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(lib().spade_policy_split(int(k_total), int(func), w, ctypes.byref(wb),
+                                    ctypes.byref(kd)))
+    radii = tuple(int(x) for x in w)
+    return (None if radii[0] < 0 else radii), int(wb.value), int(kd.value)
 
 
 def spade_attn_workspace_bytes(g: spade_geom) -> int:

@@ -312,6 +312,17 @@ def test_policy_budgets_errors():
     assert ok(NULL, 0, None, 0, 4, 10, NULL, None) == S.SPADE_OK                     # H = 0: no-op
 
 
+def test_policy_tau_errors():
+    ok = S.lib().spade_policy_tau
+    assert ok(FAKE, -1, None, 0, 0.9, FAKE, None) == S.SPADE_ERR_INVALID_ARG        # negative H
+    assert ok(FAKE, 4, None, 0, 0.0, FAKE, None) == S.SPADE_ERR_INVALID_ARG         # tau = 0
+    assert ok(FAKE, 4, None, 0, 1.5, FAKE, None) == S.SPADE_ERR_INVALID_ARG         # tau > 1
+    assert ok(FAKE, 4, None, 0, float("nan"), FAKE, None) == S.SPADE_ERR_INVALID_ARG
+    assert ok(FAKE, 4, None, 0, 0.9, NULL, None) == S.SPADE_ERR_INVALID_ARG         # null output
+    assert ok(FAKE, 4, _heads(0, 4), 2, 0.9, FAKE, None) == S.SPADE_ERR_INVALID_ARG  # head 4 >= H
+    assert ok(NULL, 0, None, 0, 0.9, NULL, None) == S.SPADE_OK                      # H = 0: no-op
+
+
 def test_multi_scheme_attention_errors():
     L = S.lib()
     g1, g2 = _g(), _g(bt=1, bh=8, bw=2)
