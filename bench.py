@@ -10,8 +10,10 @@ Hunyuan-Video 720p attention layer (B=1, H=24, d=128, grid 16x45x80, blocks
 Prints one JSON line. `value` is kept-block bf16 TFLOP/s of the whole call
 (kept matmul FLOPs / ms per call); `roofline` describes the attention kernel
 (bound by MFMA); `cpu_baseline` times the fp64 CPU oracle on a bounded sample.
-Each timed step has its own HIP event pair on the launch stream, and a read of a
-512 MiB scratch buffer between steps evicts the MALL (`--no-flush` keeps it warm).
+Each timed step has its own HIP event pair on the launch stream. The main timing
+runs the steps back to back (the MALL keeps what the previous step left, as the
+projection GEMM that writes Q, K, V leaves it in a model); a second pass with a
+512 MiB scratch write between steps is reported as `cold_mall`.
 """
 from __future__ import annotations
 
@@ -160,7 +162,7 @@ def attn_kernel_label(g) -> str:
     list fit one CU's 160 KB of LDS, the single-member kernel otherwise."""
     tiles = -(-g.bt * g.bh * g.bw // 32)
     ring = 8 * 2 * 32 * g.d * 2
-    if tiles == 5 and ring + 256 * 4 + g.NB * 4 <= 160 * 1024:
+    if tiles == 5 and ring + 256 * 4 + 8 * 4 + g.NB * 4 <= 160 * 1024:
         return "spade attn_pp_kernel (paired waves, bf16 MFMA 32x32x16)"
     return "spade attn_kernel (bf16 MFMA 32x32x16)"
 
@@ -294,8 +296,11 @@ def main():
                          "window + per-head k inversely proportional to the Selected AS)")
     ap.add_argument("--sweep", action="store_true",
                     help="run the block-shape sweep (per-head blocking choice) instead")
-    ap.add_argument("--no-flush", action="store_true",
-                    help="do not evict the MALL between timed steps")
+    ap.add_argument("--flush", default="none", choices=["write", "read", "none"],
+                    help="how the MALL is evicted between the main timed steps (a 512 MiB "
+                         "write or read); with none, a second pass with the write flush is "
+                         "reported as cold_mall")
+    ap.add_argument("--no-cold", action="store_true", help="skip the cold-MALL pass")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only run a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
@@ -345,47 +350,68 @@ def main():
     torch.cuda.synchronize()
 
     K_ = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(K_)]
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    # Between timed steps a read of a 512 MiB scratch buffer evicts the 256 MB MALL, so
-    # no step starts on inputs the previous one left in the cache (a read leaves no
-    # dirty lines whose write-back would land in the next step); each step is timed by
-    # its own event pair (the flush lies outside it).
-    flush = None if args.no_flush else torch.zeros(128 << 20, dtype=torch.float32, device=dev)
-    log(f"timing {K_} steps" + ("" if flush is None else " (MALL flushed between steps)"))
-    torch.cuda.synchronize()
-    t_host0 = time.perf_counter()
-    start.record(stream)
-    for k in range(K_):
-        if flush is not None:
-            flush.amax()
-        e = ev[k]
-        e[0].record(stream)
-        p.reorder_in(Q, K, V)
-        e[1].record(stream)
-        p.summarize()
-        e[2].record(stream)
-        p.select()
-        e[3].record(stream)
-        p.attend()
-        e[4].record(stream)
-        p.restore()
-        e[5].record(stream)
-    end.record(stream)
-    torch.cuda.synchronize()
-    t_host = time.perf_counter() - t_host0
-    ms_step = float(np.mean([ev[k][0].elapsed_time(ev[k][5]) for k in range(K_)]))
-    ms_region = start.elapsed_time(end) / K_
+
+    def timed(flush_mode):
+        """K timed steps, each with its own event pair on the launch stream. With a
+        flush mode, a 512 MiB scratch write (or read) between steps evicts the 256 MB
+        MALL first; the flush lies outside the steps' event pairs."""
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(K_)]
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        flush = None if flush_mode == "none" else torch.zeros(128 << 20, dtype=torch.float32,
+                                                              device=dev)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        start.record(stream)
+        for k in range(K_):
+            if flush is not None:
+                if flush_mode == "write":
+                    flush.fill_(float(k))
+                else:
+                    flush.amax()
+            e = ev[k]
+            e[0].record(stream)
+            p.reorder_in(Q, K, V)
+            e[1].record(stream)
+            p.summarize()
+            e[2].record(stream)
+            p.select()
+            e[3].record(stream)
+            p.attend()
+            e[4].record(stream)
+            p.restore()
+            e[5].record(stream)
+        end.record(stream)
+        torch.cuda.synchronize()
+        t_h = time.perf_counter() - t0
+        ms = float(np.mean([ev[k][0].elapsed_time(ev[k][5]) for k in range(K_)]))
+        names_ = ["reorder", "summarize", "select", "attention", "restore"]
+        st = {n: float(np.mean([ev[k][j].elapsed_time(ev[k][j + 1]) for k in range(K_)]))
+              for j, n in enumerate(names_)}
+        del flush
+        return ms, st, start.elapsed_time(end) / K_, t_h
+
+    log(f"timing {K_} steps" + ("" if args.flush == "none" else f" (MALL flush: {args.flush})"))
+    ms_step, stage_ms, _, t_host = timed(args.flush)
     names = ["reorder", "summarize", "select", "attention", "restore"]
-    stage_ms = {n: float(np.mean([ev[k][s].elapsed_time(ev[k][s + 1]) for k in range(K_)]))
-                for s, n in enumerate(names)}
-    if p.virtual:  # summaries from raster; attention reads and writes raster rows
-        stage_ms["summaries"] = stage_ms.pop("reorder") + stage_ms.pop("summarize")
-        stage_ms.pop("restore")
-        names = ["summaries", "select", "attention"]
-    elif p.fused:  # blocking of Q, K, V and the summaries are one stage
-        stage_ms["blocking_summaries"] = stage_ms.pop("reorder") + stage_ms.pop("summarize")
-        names = ["blocking_summaries", "select", "attention", "restore"]
+
+    def merge_stages(st):
+        if p.virtual:  # summaries from raster; attention reads and writes raster rows
+            st["summaries"] = st.pop("reorder") + st.pop("summarize")
+            st.pop("restore")
+            return ["summaries", "select", "attention"]
+        if p.fused:  # blocking of Q, K, V and the summaries are one stage
+            st["blocking_summaries"] = st.pop("reorder") + st.pop("summarize")
+            return ["blocking_summaries", "select", "attention", "restore"]
+        return names
+
+    names = merge_stages(stage_ms)
+    cold = None
+    if args.flush == "none" and not args.no_cold:
+        log(f"timing {K_} steps with the MALL evicted between them (512 MiB write)")
+        c_ms, c_st, _, _ = timed("write")
+        merge_stages(c_st)
+        cold = {"flush": "512 MiB write between steps", "ms_per_step": round(c_ms, 4),
+                "stage_ms": {n: round(c_st[n], 4) for n in names}}
 
     kf = kept_flops(p, nvalid)
     counts = p.counts
@@ -464,8 +490,8 @@ def main():
                              "bytes": round(sum(sb.values()))},
         "attention_share_of_call": round(stage_ms["attention"] / ms_step, 4),
         "dense_baseline": dense,
-        "mall_flushed_between_steps": flush is not None,
-        "ms_per_step_incl_flush": round(ms_region, 4),
+        "mall_flush_between_steps": args.flush,
+        "cold_mall": cold,
         "host_wall_s_timed_region": round(t_host, 3),
         "device": torch.cuda.get_device_name(0),
     }

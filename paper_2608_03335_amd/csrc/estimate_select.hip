@@ -284,8 +284,17 @@ __global__ void __launch_bounds__(kThreads)
   unsigned char* rowmark = colmark + NB;                                  // [kRows]
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i0 = blockIdx.x * kRows;
-  const int64_t bh = blockIdx.y;
+  // Workgroup w runs on XCD w % 8. The (head, row group) items are numbered head-major
+  // and each XCD takes one contiguous eighth of them, so a head's row groups share
+  // one XCD (two at a boundary) and its key summaries are fetched into that XCD's L2
+  // once instead of into every XCD's.
+  const int n_rg = (g.NB + kRows - 1) / kRows;
+  const int64_t items = int64_t(g.B) * g.H * n_rg;
+  const int64_t per_xcd = (items + 7) / 8;
+  const int64_t item = int64_t(blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (item >= items) return;  // grid padding: the whole workgroup leaves together
+  const int i0 = int(item % n_rg) * kRows;
+  const int64_t bh = item / n_rg;
   const int h = int(bh % g.H);
   const double* q0 = p.q0 + bh * NB * D;
   const double* k0 = p.k0 + bh * NB * D;
@@ -505,7 +514,8 @@ hipError_t launch_des(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
       reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
       int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 8 + kMaxSelectNB * 5 + kRows));
   if (e != hipSuccess) return e;
-  const dim3 grid((g.NB + kRows - 1) / kRows, g.B * g.H);
+  const int64_t items = int64_t(g.B) * g.H * ((g.NB + kRows - 1) / kRows);
+  const dim3 grid(unsigned((items + 7) / 8 * 8));  // see the XCD mapping in the kernel
   select_kernel<D, EST, SM><<<grid, kThreads, lds, s>>>(g, p);
   return hipGetLastError();
 }
