@@ -24,6 +24,7 @@
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  *   spade_sparse_attn_raster_multi  the same over heads with different blockings
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
+ *   spade_candidate_sics     SICS of every candidate blocking in one pass
  *   spade_aggregation_score  per-head Aggregation Score of one candidate scheme
  *   spade_choose_scheme      per-head argmax over the candidates
  *
@@ -144,6 +145,30 @@ spade_status spade_block_summarize(const spade_geom* g, const void* q, const voi
                                    void* kb, double* qbar, double* kbar, double* sics_q,
                                    double* sics_k, const int32_t* heads, int32_t n_heads,
                                    hipStream_t stream);
+
+/*
+ * SICS of every candidate blocking in one pass — paper §3.2: the head-wise scheme
+ * choice scores each candidate by Eq. (3), the sum of its blocks' SICS (Eq. (4)/(5)),
+ * for Q and for K. Reading Q and K once for all candidates: each token's unit vector
+ * is added into a cell of the candidates' common refinement, and every candidate
+ * block's sum of unit vectors is the sum of its cells.
+ *
+ *   geoms, n_geoms: the candidate blockings (1 <= n_geoms <= 8); all share B, H, d
+ *            and the grid (T, Hs, Ws).
+ *   q, k:    raster bf16 [B,H,N,d].
+ *   sics_q, sics_k: HOST arrays of n_geoms DEVICE pointers; entry c receives fp64
+ *            [B,H,NB_c], the SICS spade_block_summarize computes under geoms[c] (up
+ *            to rounding: same fp64 unit rows, summed cell by cell).
+ *   Summation orders are fixed (tokens in raster order inside a cell, cells in
+ *   (t, y, x) order inside a block): deterministic.
+ *   Returns SPADE_ERR_UNSUPPORTED when the candidates' block boundaries cut an axis
+ *   of their common region (per axis the least common multiple of the extents) into
+ *   more than 48 cells, or a region's cells need more than 144 KiB of fp64 sums
+ *   (cells x d x 8 bytes); the caller then scores the candidates one at a time.
+ */
+spade_status spade_candidate_sics(const spade_geom* geoms, int32_t n_geoms, const void* q,
+                                  const void* k, double* const* sics_q, double* const* sics_k,
+                                  hipStream_t stream);
 
 /*
  * Aggregation Score of one blocking-scheme candidate — paper §3.2, Eq. (3):

@@ -390,6 +390,107 @@ spade_status spade_policy_budgets(const double* as_best, int32_t H, const int32_
                     "policy_budgets launch");
 }
 
+spade_status spade_candidate_sics(const spade_geom* geoms, int32_t n_geoms, const void* q,
+                                  const void* k, double* const* sics_q, double* const* sics_k,
+                                  hipStream_t stream) {
+  if (!geoms || n_geoms < 1 || n_geoms > spade::kMaxCandGeoms)
+    return fail(SPADE_ERR_INVALID_ARG, "need 1..%d geometries (got %d)", spade::kMaxCandGeoms,
+                n_geoms);
+  spade::DevGeom dg[spade::kMaxCandGeoms];
+  bool empty = false;
+  for (int c = 0; c < n_geoms; ++c) {
+    bool e = false;
+    spade_status st = check_geom(&geoms[c], &dg[c], &e);
+    if (st != SPADE_OK) return st;
+    const spade_geom& a = geoms[0];
+    const spade_geom& b = geoms[c];
+    if (b.B != a.B || b.H != a.H || b.d != a.d || b.T != a.T || b.Hs != a.Hs || b.Ws != a.Ws)
+      return fail(SPADE_ERR_INVALID_ARG, "geometry %d differs from geometry 0 outside the blocking",
+                  c);
+    empty = e;
+  }
+  if (empty) return SPADE_OK;
+  if (dg[0].N * int64_t(dg[0].d) * 2 >= (int64_t(1) << 31))
+    return fail(SPADE_ERR_UNSUPPORTED, "one pass over the candidates needs N*d*2 < 2^31 bytes per head");
+  if (!q || !k || !sics_q || !sics_k)
+    return fail(SPADE_ERR_INVALID_ARG, "q, k, sics_q and sics_k must be non-null");
+  if (!aligned16(q) || !aligned16(k))
+    return fail(SPADE_ERR_INVALID_ARG, "q and k must be 16-byte aligned");
+  spade::CandPlan pl = {};
+  pl.C = n_geoms;
+  const int G3[3] = {dg[0].T, dg[0].Hs, dg[0].Ws};
+  for (int c = 0; c < n_geoms; ++c) {
+    if (!sics_q[c] || !sics_k[c])
+      return fail(SPADE_ERR_INVALID_ARG, "sics_q[%d] and sics_k[%d] must be non-null", c, c);
+    pl.sics_q[c] = sics_q[c];
+    pl.sics_k[c] = sics_k[c];
+    const int e3[3] = {dg[c].bt, dg[c].bh, dg[c].bw};
+    const int n3[3] = {dg[c].nT, dg[c].nH, dg[c].nW};
+    for (int a = 0; a < 3; ++a) {
+      pl.ext[c][a] = e3[a];
+      pl.nblk[c][a] = n3[a];
+    }
+  }
+  int64_t cells = 1;
+  for (int a = 0; a < 3; ++a) {
+    // region extent: the least common multiple of the candidates' extents on this axis
+    int64_t L = 1;
+    for (int c = 0; c < n_geoms; ++c) {
+      int64_t x = L, y = pl.ext[c][a];
+      while (y) { const int64_t t = x % y; x = y; y = t; }
+      L = L / x * pl.ext[c][a];
+      if (L > (int64_t(1) << 20)) break;
+    }
+    // cells: the union of the candidates' block boundaries inside [0, L)
+    int n = 0;
+    for (int64_t p = 0; p < L && n <= spade::kMaxCellsAxis; ++p) {
+      bool cut = false;
+      for (int c = 0; c < n_geoms; ++c) cut = cut || p % pl.ext[c][a] == 0;
+      if (cut) {
+        if (n < spade::kMaxCellsAxis) pl.start[a][n] = int(p);
+        ++n;
+      }
+    }
+    if (L > (int64_t(1) << 20) || n > spade::kMaxCellsAxis)
+      return fail(SPADE_ERR_UNSUPPORTED,
+                  "candidate blockings cut axis %d into more than %d cells per region", a,
+                  spade::kMaxCellsAxis);
+    pl.L[a] = int(L);
+    pl.start[a][n] = int(L);
+    pl.ncell[a] = n;
+    pl.R[a] = int((G3[a] + L - 1) / L);
+    cells *= n;
+    for (int c = 0; c < n_geoms; ++c)  // cell index of each block boundary j * ext
+      for (int j = 0, i = 0; j <= int(L / pl.ext[c][a]); ++j) {
+        while (i < n && pl.start[a][i] < j * pl.ext[c][a]) ++i;
+        pl.bnd[c][a][j] = static_cast<unsigned char>(i);
+      }
+  }
+  if (cells * dg[0].d * int64_t(sizeof(double)) > spade::kMaxCellLds)
+    return fail(SPADE_ERR_UNSUPPORTED, "%lld cells per region exceed the LDS (%d bytes)",
+                (long long)cells, spade::kMaxCellLds);
+  {  // cells by token count in a full region, largest first (ties: lower index)
+    const int nc = int(cells);
+    auto size = [&](int c) {
+      const int cx = c % pl.ncell[2], cy = (c / pl.ncell[2]) % pl.ncell[1];
+      const int ct = c / (pl.ncell[2] * pl.ncell[1]);
+      return (pl.start[0][ct + 1] - pl.start[0][ct]) * (pl.start[1][cy + 1] - pl.start[1][cy]) *
+             (pl.start[2][cx + 1] - pl.start[2][cx]);
+    };
+    for (int c = 0; c < nc; ++c) pl.order[c] = static_cast<unsigned short>(c);
+    for (int a = 1; a < nc; ++a)  // insertion sort: stable, at most a few hundred cells
+      for (int b = a; b > 0 && size(pl.order[b]) > size(pl.order[b - 1]); --b) {
+        const unsigned short t = pl.order[b];
+        pl.order[b] = pl.order[b - 1];
+        pl.order[b - 1] = t;
+      }
+  }
+  if (int64_t(pl.R[0]) * pl.R[1] * pl.R[2] > (int64_t(1) << 31) - 1)
+    return fail(SPADE_ERR_UNSUPPORTED, "too many regions");
+  return hip_status(spade::launch_candidate_sics(dg[0], pl, q, k, stream),
+                    "candidate_sics launch");
+}
+
 spade_status spade_policy_tau(const double* as_best, int32_t H, const int32_t* heads,
                               int32_t n_heads, double tau, double* tau_out, hipStream_t stream) {
   if (H < 0 || H > 65535) return fail(SPADE_ERR_INVALID_ARG, "H must lie in [0, 65535] (got %d)", H);

@@ -116,6 +116,29 @@ struct SelectSpec {
   double* scores;
 };
 hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
+
+// SICS of every candidate blocking in one pass over the raster Q and K. A region is
+// the per-axis least common multiple of the candidates' block extents, so every
+// candidate block lies in one region; within a region the union of the candidates'
+// block boundaries cuts each axis into cells. The plan (host-built, passed by value)
+// gives the cell starts per axis and, per candidate and axis, the cell index of each
+// of its block boundaries inside a region.
+constexpr int kMaxCandGeoms = 8;
+constexpr int kMaxCellsAxis = 48;
+constexpr int kMaxCellLds = 144 * 1024;  // fp64 cell sums of one region (d per cell)
+struct CandPlan {
+  int C;
+  int L[3], R[3], ncell[3];         // region extent, regions, cells per axis (t, y, x)
+  int start[3][kMaxCellsAxis + 1];  // cell starts inside a region (start[a][ncell] = L)
+  int ext[kMaxCandGeoms][3];        // block extents per candidate
+  int nblk[kMaxCandGeoms][3];       // blocks per axis of the whole grid
+  unsigned char bnd[kMaxCandGeoms][3][kMaxCellsAxis + 1];  // boundary j -> cell index
+  unsigned short order[kMaxCellLds / (64 * 8)];  // cells by token count, largest first
+  double* sics_q[kMaxCandGeoms];
+  double* sics_k[kMaxCandGeoms];
+};
+hipError_t launch_candidate_sics(const DevGeom& g, const CandPlan& plan, const void* q,
+                                 const void* k, hipStream_t s);
 hipError_t launch_policy_tau(const double* as_best, const HeadMap& hm, double tau,
                              double* tau_out, hipStream_t s);
 bool policy_dense(int step, int n_steps, int task, bool turbo);

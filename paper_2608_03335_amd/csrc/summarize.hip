@@ -404,7 +404,165 @@ __global__ void __launch_bounds__(kThreads) choose_scheme_kernel(const double* _
   if (best) best[h] = top;
 }
 
+// SICS of every candidate blocking in one pass (the head-wise scheme choice of §3.2
+// evaluates each candidate's Eq. (3) score; this reads Q and K once for all of them).
+// One workgroup per (region, batch x head, tensor). Phase 1: each group of V lanes
+// (one token row, 8 columns per lane) walks whole cells in raster order, summing the
+// unit rows in fp64, and parks each cell's sum in LDS. Phase 2: each candidate block
+// of the region is the sum of its cells in (t, y, x) cell order; its SICS is that
+// sum's squared norm. Both orders are fixed, so the result is deterministic.
+constexpr int kCandThreads = 512;
+constexpr int kCandBatch = 8;  // token rows in flight per lane group
+
+template <int D>
+__global__ void __launch_bounds__(kCandThreads)
+    candidate_sics_kernel(DevGeom g, CandPlan pl, const uint4* __restrict__ q,
+                          const uint4* __restrict__ k) {
+  constexpr int V = D / 8;
+  constexpr int NG = kCandThreads / V;  // lane groups
+  extern __shared__ double cell_sum[];  // [cells][D]
+  __shared__ int next_cell;
+  const int vec = threadIdx.x % V, grp = threadIdx.x / V;
+  const int reg = blockIdx.x;
+  const int rx = reg % pl.R[2], ry = (reg / pl.R[2]) % pl.R[1], rt = reg / (pl.R[2] * pl.R[1]);
+  const int o[3] = {rt * pl.L[0], ry * pl.L[1], rx * pl.L[2]};
+  const int G3[3] = {g.T, g.Hs, g.Ws};
+  const int64_t bh = blockIdx.y;
+  const uint4* src = (blockIdx.z ? k : q) + bh * g.N * V;
+  const int ncells = pl.ncell[0] * pl.ncell[1] * pl.ncell[2];
+
+  // phase 1: cell sums. Groups take cells from a shared counter, largest first, so
+  // the groups finish together; a cell is always summed by one group in raster
+  // order, so the result does not depend on which group takes it.
+  if (threadIdx.x == 0) next_cell = 0;
+  __syncthreads();
+  const int leader = (threadIdx.x & 63) & ~(V - 1);  // first lane of this group in the wave
+  for (;;) {
+    int w = 0;
+    if (vec == 0) w = atomicAdd(&next_cell, 1);
+    w = __shfl(w, leader, 64);
+    if (w >= ncells) break;
+    const int c = pl.order[w];
+    const int cx = c % pl.ncell[2], cy = (c / pl.ncell[2]) % pl.ncell[1];
+    const int ct = c / (pl.ncell[2] * pl.ncell[1]);
+    const int lo[3] = {o[0] + pl.start[0][ct], o[1] + pl.start[1][cy], o[2] + pl.start[2][cx]};
+    int ex[3];
+    ex[0] = max(0, min(o[0] + pl.start[0][ct + 1], G3[0]) - lo[0]);
+    ex[1] = max(0, min(o[1] + pl.start[1][cy + 1], G3[1]) - lo[1]);
+    ex[2] = max(0, min(o[2] + pl.start[2][cx + 1], G3[2]) - lo[2]);
+    const int n = ex[0] * ex[1] * ex[2];
+    double uacc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) uacc[e] = 0.0;
+    // walk the cell in raster order with a carry counter (no divisions); rows past the
+    // cell re-read its first row and are replaced by zeros, which add nothing
+    int pt = 0, py = 0, px = 0;
+    const uint32_t base0 = (uint32_t(lo[0]) * g.Hs + lo[1]) * g.Ws + lo[2];
+    auto fetch = [&](int s0, uint4 (&v)[kCandBatch]) {
+#pragma unroll
+      for (int r = 0; r < kCandBatch; ++r) {
+        const bool live = s0 + r < n;
+        // 32-bit offsets: one head's rows span < 2^31 bytes (checked on the host)
+        const uint32_t tok = live ? base0 + (uint32_t(pt) * g.Hs + py) * g.Ws + px : base0;
+        const uint4 x = src[tok * V + vec];
+        v[r] = live ? x : make_uint4(0, 0, 0, 0);
+        if (++px == ex[2]) {
+          px = 0;
+          if (++py == ex[1]) {
+            py = 0;
+            ++pt;
+          }
+        }
+      }
+    };
+    // two batches in flight: the next batch's loads are issued before this one is summed
+    uint4 va[kCandBatch], vb[kCandBatch];
+    if (n > 0) fetch(0, va);
+    for (int s0 = 0; s0 < n; s0 += 2 * kCandBatch) {
+      if (s0 + kCandBatch < n) fetch(s0 + kCandBatch, vb);
+#pragma unroll
+      for (int r = 0; r < kCandBatch; ++r) {
+        float f[8];
+        bf16x8_to_f32(va[r], f);  // rows past the cell are zero and add nothing
+        add_unit_row<V>(f, uacc);
+        __builtin_amdgcn_sched_barrier(0);  // one row at a time: few live temporaries
+      }
+      if (s0 + 2 * kCandBatch < n) fetch(s0 + 2 * kCandBatch, va);
+      if (s0 + kCandBatch < n) {
+#pragma unroll
+        for (int r = 0; r < kCandBatch; ++r) {
+          float f[8];
+          bf16x8_to_f32(vb[r], f);
+          add_unit_row<V>(f, uacc);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) cell_sum[c * D + vec * 8 + e] = uacc[e];
+  }
+  __syncthreads();
+
+  // phase 2: candidate blocks of this region
+  auto nb = [&](int ci) {
+    return (pl.L[0] / pl.ext[ci][0]) * (pl.L[1] / pl.ext[ci][1]) * (pl.L[2] / pl.ext[ci][2]);
+  };
+  int total = 0;
+  for (int ci = 0; ci < pl.C; ++ci) total += nb(ci);
+  for (int w = grp; w < total; w += NG) {
+    int ci = 0, j = w;
+    while (j >= nb(ci)) j -= nb(ci++);
+    const int px = pl.L[2] / pl.ext[ci][2], py = pl.L[1] / pl.ext[ci][1];
+    const int jx = j % px, jy = (j / px) % py, jt = j / (px * py);
+    const int bt = o[0] / pl.ext[ci][0] + jt, by = o[1] / pl.ext[ci][1] + jy;
+    const int bx = o[2] / pl.ext[ci][2] + jx;
+    if (bt >= pl.nblk[ci][0] || by >= pl.nblk[ci][1] || bx >= pl.nblk[ci][2]) continue;
+    double u[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) u[e] = 0.0;
+    for (int ct = pl.bnd[ci][0][jt]; ct < pl.bnd[ci][0][jt + 1]; ++ct)
+      for (int cy = pl.bnd[ci][1][jy]; cy < pl.bnd[ci][1][jy + 1]; ++cy)
+        for (int cx = pl.bnd[ci][2][jx]; cx < pl.bnd[ci][2][jx + 1]; ++cx) {
+          const double* cs = cell_sum + ((ct * pl.ncell[1] + cy) * pl.ncell[2] + cx) * D + vec * 8;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) u[e] += cs[e];
+        }
+    double ss = 0.0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ss += u[e] * u[e];
+    ss = row_group_sum<V>(ss);
+    if (vec == 0) {
+      const int NBc = pl.nblk[ci][0] * pl.nblk[ci][1] * pl.nblk[ci][2];
+      const int64_t blk = (int64_t(bt) * pl.nblk[ci][1] + by) * pl.nblk[ci][2] + bx;
+      (blockIdx.z ? pl.sics_k[ci] : pl.sics_q[ci])[bh * NBc + blk] = ss;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_candidate_sics(const DevGeom& g, const CandPlan& plan, const void* q,
+                                 const void* k, hipStream_t s) {
+  const int ncells = plan.ncell[0] * plan.ncell[1] * plan.ncell[2];
+  const size_t lds = size_t(ncells) * g.d * sizeof(double);
+  const dim3 grid(unsigned(plan.R[0] * plan.R[1] * plan.R[2]), unsigned(g.B * g.H), 2);
+  const uint4* q4 = static_cast<const uint4*>(q);
+  const uint4* k4 = static_cast<const uint4*>(k);
+  if (g.d == 128) {
+    const hipError_t e = ensure_dynamic_lds(
+        reinterpret_cast<const void*>(&candidate_sics_kernel<128>), kMaxCellLds);
+    if (e != hipSuccess) return e;
+    candidate_sics_kernel<128><<<grid, kCandThreads, lds, s>>>(g, plan, q4, k4);
+  } else if (g.d == 64) {
+    const hipError_t e = ensure_dynamic_lds(
+        reinterpret_cast<const void*>(&candidate_sics_kernel<64>), kMaxCellLds);
+    if (e != hipSuccess) return e;
+    candidate_sics_kernel<64><<<grid, kCandThreads, lds, s>>>(g, plan, q4, k4);
+  } else {
+    return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_choose_scheme(const double* as_qk, int C, int B, int H, int* choice,
                                 double* best, hipStream_t s) {

@@ -203,7 +203,7 @@ class SweepPath:
     """
 
     def __init__(self, B, H, d, T, Hs, Ws, candidates, sparsity, *, scale=None, device="cuda",
-                 policy=None, raster=False, tau=None):
+                 policy=None, raster=False, tau=None, one_pass=True):
         self.B, self.H, self.d = B, H, d
         self.raster = bool(raster)
         if self.raster and H > S.MAX_HEAD_LIST:
@@ -213,6 +213,8 @@ class SweepPath:
         # Top-P with mass tau (the policy then spreads the mass over the heads, and the
         # Top-K budget only sizes its static window)
         self.tau = None if tau is None else float(tau)
+        # candidate evaluation in one pass over Q and K (spade_candidate_sics)
+        self.one_pass = bool(one_pass)
         self.shapes = [tuple(c) for c in candidates]
         self.sparsity = float(sparsity)
         self.scale = float(scale if scale is not None else 1.0 / math.sqrt(d))
@@ -249,8 +251,22 @@ class SweepPath:
         self.O = torch.empty((B, H, T * Hs * Ws, d), dtype=bf, device=dev)
 
     def evaluate(self, Q, K, stream=None):
+        """SICS of every candidate (one pass over Q and K when the candidates' common
+        refinement fits, else one pass per candidate), the Aggregation Scores, and the
+        per-head choice."""
+        if self.one_pass:
+            try:
+                S.spade_candidate_sics(self.geoms, Q, K, [e["sics_q"] for e in self.ev],
+                                       [e["sics_k"] for e in self.ev], stream=stream)
+            except S.SpadeError as err:
+                if err.status != S.SPADE_ERR_UNSUPPORTED:
+                    raise
+                self.one_pass = False
+        if not self.one_pass:
+            for g, e in zip(self.geoms, self.ev):
+                S.spade_block_summarize(g, Q, K, sics_q=e["sics_q"], sics_k=e["sics_k"],
+                                        stream=stream)
         for c, (g, e) in enumerate(zip(self.geoms, self.ev)):
-            S.spade_block_summarize(g, Q, K, sics_q=e["sics_q"], sics_k=e["sics_k"], stream=stream)
             S.spade_aggregation_score(g, e["sics_q"], e["sics_k"], self.as_qk[c], stream=stream)
         S.spade_choose_scheme(self.as_qk, self.choice, self.best, stream=stream)
 

@@ -28,7 +28,7 @@ SPADE_INTRA_NONE, SPADE_INTRA_THRESHOLD, SPADE_INTRA_TOPK = 0, 1, 2
 SPADE_TASK_T2V, SPADE_TASK_I2V = 0, 1
 
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
-            "spade_aggregation_score",
+            "spade_candidate_sics", "spade_aggregation_score",
             "spade_choose_scheme", "spade_estimate_select", "spade_block_minmax",
             "spade_compose_select", "spade_policy_budgets", "spade_policy_tau",
             "spade_policy_dense", "spade_policy_split", "spade_attn_workspace_bytes",
@@ -104,6 +104,8 @@ def lib() -> ctypes.CDLL:
             "spade_block_summarize": (i32, [G, vp, vp, vp, vp, vp, vp, vp, vp,
                                             ctypes.POINTER(i32), i32, vp]),
             "spade_aggregation_score": (i32, [G, vp, vp, vp, vp, vp, vp]),
+            "spade_candidate_sics": (i32, [G, i32, vp, vp, ctypes.POINTER(vp), ctypes.POINTER(vp),
+                                           vp]),
             "spade_choose_scheme": (i32, [vp, i32, i32, i32, vp, vp, vp]),
             "spade_estimate_select": (i32, [G, vp, vp, i32, i32, f64, f64, vp, vp, vp, vp]),
             "spade_block_minmax": (i32, [G, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -245,6 +247,26 @@ def spade_block_summarize(g: spade_geom, q, k, qb=None, kb=None, qbar=None, kbar
                  a(kb, BF16, D.blocked, "kb"), a(qbar, F64, D.summ, "qbar"),
                  a(kbar, F64, D.summ, "kbar"), a(sics_q, F64, D.per_block, "sics_q"),
                  a(sics_k, F64, D.per_block, "sics_k"), arr, n, stream))
+
+
+def spade_candidate_sics(geoms, q, k, sics_q, sics_k, stream=None):
+    """geoms: sequence of spade_geom; sics_q / sics_k: per candidate a fp64 [B,H,NB_c]
+    device tensor. Raises SpadeError(SPADE_ERR_UNSUPPORTED) when the candidates'
+    common refinement does not fit (score them one at a time then)."""
+    a = _Args()
+    if len(sics_q) != len(geoms) or len(sics_k) != len(geoms):
+        raise SpadeError(SPADE_ERR_INVALID_ARG, "one sics_q and one sics_k tensor per geometry")
+    ga = (spade_geom * max(len(geoms), 1))(*geoms)
+    D = _Dims(geoms[0]) if len(geoms) else None
+    pq = (ctypes.c_void_p * max(len(geoms), 1))(
+        *[_value(a(t, F64, _Dims(g).per_block, f"sics_q[{c}]")) for c, (g, t) in
+          enumerate(zip(geoms, sics_q))])
+    pk = (ctypes.c_void_p * max(len(geoms), 1))(
+        *[_value(a(t, F64, _Dims(g).per_block, f"sics_k[{c}]")) for c, (g, t) in
+          enumerate(zip(geoms, sics_k))])
+    _check(a.run(lib().spade_candidate_sics, ga, len(geoms),
+                 a(q, BF16, D.raster if D else None, "q"), a(k, BF16, D.raster if D else None, "k"),
+                 pq, pk, stream))
 
 
 def spade_aggregation_score(g: spade_geom, sics_q, sics_k, as_qk, as_q=None, as_k=None,

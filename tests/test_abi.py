@@ -312,6 +312,31 @@ def test_policy_budgets_errors():
     assert ok(NULL, 0, None, 0, 4, 10, NULL, None) == S.SPADE_OK                     # H = 0: no-op
 
 
+def test_candidate_sics_errors():
+    L = S.lib()
+    fn = L.spade_candidate_sics
+    P2 = (ctypes.c_void_p * 2)(0x1000, 0x1000)
+    g1, g2 = _g(), _g(bt=1, bh=8, bw=2)
+    two = (S.spade_geom * 2)(g1, g2)
+    assert fn(two, 0, FAKE, FAKE, P2, P2, None) == S.SPADE_ERR_INVALID_ARG      # no geometry
+    assert fn(two, 9, FAKE, FAKE, P2, P2, None) == S.SPADE_ERR_INVALID_ARG      # above 8
+    other = (S.spade_geom * 2)(g1, _g(T=5, bt=1, bh=8, bw=2))
+    assert fn(other, 2, FAKE, FAKE, P2, P2, None) == S.SPADE_ERR_INVALID_ARG    # grids differ
+    assert fn(two, 2, NULL, FAKE, P2, P2, None) == S.SPADE_ERR_INVALID_ARG      # null q
+    assert fn(two, 2, MISALIGNED, FAKE, P2, P2, None) == S.SPADE_ERR_INVALID_ARG
+    P0 = (ctypes.c_void_p * 2)(0x1000, 0)
+    assert fn(two, 2, FAKE, FAKE, P0, P2, None) == S.SPADE_ERR_INVALID_ARG      # null sics_q[1]
+    # pairwise coprime extents: the common region is cut into too many cells
+    big = _g(T=64, Hs=64, Ws=64)
+    coprime = (S.spade_geom * 4)(*[S.spade_geom(1, 2, 128, 64, 64, 64, e, 1, 1) for e in (7, 11, 13, 17)])
+    st, msg = _status(fn, coprime, 4, FAKE, FAKE, (ctypes.c_void_p * 4)(*[0x1000] * 4),
+                      (ctypes.c_void_p * 4)(*[0x1000] * 4), None)
+    assert st == S.SPADE_ERR_UNSUPPORTED and "cells" in msg, msg
+    del big
+    empty = (S.spade_geom * 1)(_g(B=0))
+    assert fn(empty, 1, NULL, NULL, NULL, NULL, None) == S.SPADE_OK              # empty: no-op
+
+
 def test_policy_tau_errors():
     ok = S.lib().spade_policy_tau
     assert ok(FAKE, -1, None, 0, 0.9, FAKE, None) == S.SPADE_ERR_INVALID_ARG        # negative H

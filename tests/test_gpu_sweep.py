@@ -272,3 +272,103 @@ def test_sweep_raster_multi_equals_grouped(case):
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
     if case == "small_pair_b2":  # some head ran on a 160-slot blocking
         assert any(int(c) < 3 for c in pb.choice.cpu())
+
+
+# ---------------- one-pass candidate evaluation (spade_candidate_sics) ----------------
+def _cand_sics(geoms, Q, K):
+    sq = [torch.full((g.B, g.H, g.NB), float("nan"), dtype=torch.float64, device=DEV) for g in geoms]
+    sk = [torch.full_like(t, float("nan")) for t in sq]
+    S.spade_candidate_sics(geoms, Q, K, sq, sk)
+    torch.cuda.synchronize()
+    return sq, sk
+
+
+@pytest.mark.parametrize("case", ["hunyuan_like_small", "ragged_d64_b2", "single", "mixed_ragged"])
+def test_candidate_sics_matches_oracle_and_per_candidate_pass(case):
+    """Every candidate's SICS from the one-pass call equals the oracle's closed form
+    (rtol 1e-9) and the per-candidate pass of spade_block_summarize (rtol 1e-12);
+    every output element is written (NaN-poisoned before)."""
+    if case == "hunyuan_like_small":
+        cfg, cands = P.small_cfg(16, 45, 24, 1, 1, 1, d=128, H=2), [(2, 8, 8), (4, 4, 8), (4, 5, 8), (8, 5, 4)]
+    elif case == "ragged_d64_b2":
+        cfg, cands = P.small_cfg(7, 13, 11, 1, 1, 1, d=64, H=3, B=2), [(2, 4, 4), (3, 4, 5), (2, 8, 2)]
+    elif case == "single":
+        cfg, cands = P.small_cfg(5, 9, 10, 1, 1, 1, d=128, H=2), [(2, 3, 4)]
+    else:
+        cfg, cands = P.small_cfg(6, 10, 15, 1, 1, 1, d=128, H=2), [(2, 3, 6), (4, 3, 3), (1, 6, 2)]
+    _say("candidate sics", case)
+    Q, K, _ = P.bf16_inputs(cfg)
+    geoms = [_geom(cfg, shape=c) for c in cands]
+    sq, sk = _cand_sics(geoms, Q, K)
+    q, k = P.to_np64(Q), P.to_np64(K)
+    for c, g in enumerate(geoms):
+        og = O.Geometry(cfg["T"], cfg["Hs"], cfg["Ws"], *cands[c])
+        for got, X in ((sq[c], q), (sk[c], k)):
+            a = got.cpu().numpy()
+            assert np.all(np.isfinite(a))
+            np.testing.assert_allclose(a, O.block_sics(O.reorder(X, og), og), rtol=1e-9, atol=1e-9)
+        pq = torch.empty_like(sq[c])
+        pk = torch.empty_like(sk[c])
+        S.spade_block_summarize(g, Q, K, sics_q=pq, sics_k=pk)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(sq[c].cpu().numpy(), pq.cpu().numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(sk[c].cpu().numpy(), pk.cpu().numpy(), rtol=1e-12, atol=1e-12)
+    again_q, again_k = _cand_sics(geoms, Q, K)
+    for c in range(len(geoms)):  # fixed summation orders: bit for bit
+        assert torch.equal(again_q[c], sq[c]) and torch.equal(again_k[c], sk[c])
+
+
+def test_candidate_sics_full_hunyuan_sweep():
+    """The sweep's four candidates at the Hunyuan-Video layer in one pass: against the
+    per-candidate pass on every block of every head, the oracle on two heads, and the
+    choice the sweep path makes with either evaluation."""
+    cfg = workload("hunyuan_sweep")
+    _say("candidate sics full hunyuan")
+    Q, K, V = P.bf16_inputs(cfg)
+    geoms = [_geom(cfg, shape=c) for c in SWEEP_CANDIDATES]
+    sq, sk = _cand_sics(geoms, Q, K)
+    for c, g in enumerate(geoms):
+        pq, pk = torch.empty_like(sq[c]), torch.empty_like(sk[c])
+        S.spade_block_summarize(g, Q, K, sics_q=pq, sics_k=pk)
+        torch.cuda.synchronize()
+        np.testing.assert_allclose(sq[c].cpu().numpy(), pq.cpu().numpy(), rtol=1e-12, atol=1e-12)
+        np.testing.assert_allclose(sk[c].cpu().numpy(), pk.cpu().numpy(), rtol=1e-12, atol=1e-12)
+        og = O.Geometry(cfg["T"], cfg["Hs"], cfg["Ws"], *SWEEP_CANDIDATES[c])
+        for h in (0, cfg["H"] - 1):
+            ref = O.block_sics(O.reorder(P.to_np64(Q[:, h:h + 1]), og), og)
+            np.testing.assert_allclose(sq[c].cpu().numpy()[:, h:h + 1], ref, rtol=1e-9, atol=1e-9)
+    one = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], SWEEP_CANDIDATES,
+                    0.85, device=DEV)
+    per = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], SWEEP_CANDIDATES,
+                    0.85, device=DEV, one_pass=False)
+    one.evaluate(Q, K)
+    per.evaluate(Q, K)
+    torch.cuda.synchronize()
+    assert one.one_pass
+    np.testing.assert_allclose(one.as_qk.cpu().numpy(), per.as_qk.cpu().numpy(), rtol=1e-12, atol=0)
+    _check_choice(one.as_qk.cpu().numpy(), per.as_qk.cpu().numpy(), one.choice.cpu().numpy())
+
+
+def test_candidate_sics_unsupported_falls_back():
+    """Candidates whose common refinement exceeds the LDS are rejected with
+    SPADE_ERR_UNSUPPORTED (nothing written); the sweep path then scores them one at a
+    time and still matches the oracle's Aggregation Scores."""
+    cfg = P.small_cfg(7, 11, 13, 1, 1, 1, d=128, H=2)
+    cands = [(1, 1, 1), (7, 5, 7)]  # 7 x 5 x 7 cells of 1 KiB of fp64 sums per region
+    _say("candidate sics fallback")
+    Q, K, _ = P.bf16_inputs(cfg)
+    geoms = [_geom(cfg, shape=c) for c in cands]
+    sq = [torch.full((g.B, g.H, g.NB), -5.0, dtype=torch.float64, device=DEV) for g in geoms]
+    sk = [torch.full_like(t, -5.0) for t in sq]
+    with pytest.raises(S.SpadeError) as e:
+        S.spade_candidate_sics(geoms, Q, K, sq, sk)
+    assert e.value.status == S.SPADE_ERR_UNSUPPORTED
+    torch.cuda.synchronize()
+    assert all(bool((t == -5.0).all()) for t in sq + sk)
+    p = SweepPath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cands, 0.5, device=DEV)
+    p.evaluate(Q, K)
+    torch.cuda.synchronize()
+    assert not p.one_pass
+    q, k = P.to_np64(Q), P.to_np64(K)
+    ref = np.stack([O.scheme_scores(q, k, O.Geometry(cfg["T"], cfg["Hs"], cfg["Ws"], *c)) for c in cands])
+    np.testing.assert_allclose(p.as_qk.cpu().numpy(), ref, rtol=AS_REL, atol=0)
