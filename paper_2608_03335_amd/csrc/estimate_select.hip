@@ -4,7 +4,9 @@
 // scores broadcast and OR-combined with the inter ones, the result united with
 // the window and sink masks), on gfx950.
 //
-// One workgroup (8 waves) owns 16 query-block rows of one head.
+// One workgroup (4 waves) owns 12 query-block rows of one head (the MFMA tiles of
+// phase 1 span 16 rows; the 4 past the item are computed and dropped). Small
+// workgroups keep three per CU, so a layer's items fit one round (Hunyuan: 720 items).
 //  1. Scores, the 16 x NB tile parked in LDS, in fp64:
 //     MEAN  S = qbar kbar^T * scale with v_mfma_f64_16x16x4. The contraction
 //           index is permuted so each lane streams 16-byte pieces of the rows.
@@ -35,8 +37,8 @@
 namespace spade {
 namespace {
 
-constexpr int kRows = 16;
-constexpr int kWaves = 8;
+constexpr int kRows = 12;
+constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 // Register slots per lane of a row's keys (element e = 64 s + lane): SM slots
 // hold rows of up to 64 SM blocks; launches pick the smallest of 4, 8, 16.
@@ -270,7 +272,8 @@ __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, in
 }
 
 // Rows of up to 512 blocks (SM <= 8) fit in 128 VGPRs outside the DSA estimator:
-// four waves per SIMD, two workgroups per CU.
+// up to four waves per SIMD; the LDS (12 score rows + histograms) allows three
+// workgroups per CU.
 template <int D, int EST, int SM>
 __global__ void __launch_bounds__(kThreads)
     __attribute__((amdgpu_waves_per_eu(SM <= 8 && EST != kEstDsa ? 4 : 1)))
@@ -353,10 +356,10 @@ __global__ void __launch_bounds__(kThreads)
       if (col < NB) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {  // acc[r] = S[4r + g4][r16]
-          const int rr = 4 * r + g4;
+          const int rr = 4 * r + g4;  // tile rows past kRows belong to the next item
           const double s = acc[r] * p.scale + 0.0;  // + 0.0 folds -0 into +0
-          sc[rr * NB + col] = s;
-          if (p.scores && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
+          if (rr < kRows) sc[rr * NB + col] = s;
+          if (p.scores && rr < kRows && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
         }
       }
     }
@@ -388,8 +391,8 @@ __global__ void __launch_bounds__(kThreads)
         for (int r = 0; r < 4; ++r) {
           const int rr = 4 * r + g4;
           const double s = acc[r] * p.scale + 0.0;
-          sc[rr * NB + col] = s;
-          if (p.scores && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
+          if (rr < kRows) sc[rr * NB + col] = s;
+          if (p.scores && rr < kRows && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = s;
         }
       }
     }
