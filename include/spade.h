@@ -21,6 +21,7 @@
  *   spade_policy_dense       the policy's dense warm-up schedule (host)
  *   spade_policy_split       the policy's static/dynamic budget split (host)
  *   spade_block_sparse_attn  flash block-sparse attention, Eq. (2)
+ *   spade_validate_lists     check of block lists (debug aid)
  *   spade_sparse_attn_raster the same on raster tensors (blocking applied on read)
  *   spade_sparse_attn_raster_multi  the same over heads with different blockings
  * and the head-wise blocking-scheme choice (§3.2, Eq. (3)):
@@ -378,6 +379,28 @@ spade_status spade_policy_dense(int32_t step, int32_t n_steps, int32_t task, int
  */
 spade_status spade_policy_split(int32_t k_total, int32_t func, int32_t* window,
                                 int32_t* window_blocks, int32_t* k_dyn);
+
+/*
+ * Check of block lists (a debug aid; the attention calls accept any lists and skip
+ * what is malformed). The lists are the block mask in the row-wise sparse form the
+ * attention walks (§3.3 optimisation (3)): per query block, the kept key blocks in
+ * ascending order. Each row (b, h, i) passes when 0 <= counts <= NB and its listed
+ * indices lie in [0, NB) and strictly ascend.
+ *
+ *   counts, indices: int32 [B,H,NB] and [B,H,NB,NB], as spade_estimate_select writes.
+ *   report:  out, device int32[4]: [0] the number of failing rows; [1] the lowest
+ *            failing row, numbered (b*H + h)*NB + i (INT32_MAX when none); [2] the
+ *            OR of the failure bits of every failing row (SPADE_LIST_*); [3] 0.
+ *            Written on `stream` by two launches (a clear, then the check).
+ *   Errors: as for every call, the geometry's (SPADE_ERR_INVALID_ARG,
+ *           SPADE_ERR_UNSUPPORTED); SPADE_ERR_INVALID_ARG for a null pointer (counts
+ *           and indices may be null for an empty problem, report may not);
+ *           SPADE_ERR_UNSUPPORTED when B*H*NB exceeds 2^31 - 1. For an empty problem
+ *           the report is still written (no failing rows).
+ */
+enum { SPADE_LIST_BAD_COUNT = 1, SPADE_LIST_BAD_INDEX = 2, SPADE_LIST_NOT_ASCENDING = 4 };
+spade_status spade_validate_lists(const spade_geom* g, const int32_t* counts,
+                                  const int32_t* indices, int32_t* report, hipStream_t stream);
 
 /*
  * Scratch bytes spade_block_sparse_attn and spade_sparse_attn_raster need for

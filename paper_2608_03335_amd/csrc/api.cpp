@@ -663,4 +663,21 @@ spade_status spade_sparse_attn_raster_noalloc(const spade_geom* g, const void* q
   return sparse_attn(g, q, k, v, counts, indices, scale, o, lse, ws, ws_bytes, true, stream);
 }
 
+spade_status spade_validate_lists(const spade_geom* g, const int32_t* counts,
+                                  const int32_t* indices, int32_t* report, hipStream_t stream) {
+  spade::DevGeom dg;
+  bool empty = false;
+  spade_status st = check_geom(g, &dg, &empty);
+  if (st != SPADE_OK) return st;
+  if (!report) return fail(SPADE_ERR_INVALID_ARG, "report must be non-null");
+  const int64_t rows = empty ? 0 : int64_t(dg.B) * dg.H * dg.NB;
+  if (rows > INT32_MAX)
+    return fail(SPADE_ERR_UNSUPPORTED, "B*H*NB = %lld rows exceeds 2^31 - 1", (long long)rows);
+  if (rows > 0 && (!counts || !indices))
+    return fail(SPADE_ERR_INVALID_ARG, "counts and indices must be non-null");
+  return hip_status(spade::launch_validate_lists(empty ? 0 : dg.NB, int(rows), counts, indices,
+                                                 report, stream),
+                    "validate_lists launch");
+}
+
 }  // extern "C"

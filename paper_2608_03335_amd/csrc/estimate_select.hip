@@ -32,6 +32,8 @@
 //     the same radix cut), when it lies in the query block's window, or when it
 //     holds one of the first `sink` raster tokens. Kept indices are written
 //     ascending.
+#include <climits>
+
 #include "spade_internal.h"
 
 namespace spade {
@@ -546,6 +548,58 @@ hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
   if (g.d == 128) return launch_d<128>(g, p, s);
   if (g.d == 64) return launch_d<64>(g, p, s);
   return hipErrorInvalidValue;
+}
+
+}  // namespace spade
+
+// Checks of block lists in the layout select_kernel writes (a debug aid: the
+// attention kernels accept any lists). One wave per row (b, h, i); a failing row
+// adds itself to the report with vector-memory atomics.
+namespace spade {
+namespace {
+
+__global__ void __launch_bounds__(64) clear_report_kernel(int* __restrict__ report) {
+  if (threadIdx.x < 4) report[threadIdx.x] = threadIdx.x == 1 ? INT_MAX : 0;
+}
+
+__global__ void __launch_bounds__(256) validate_lists_kernel(int NB, int rows,
+                                                             const int* __restrict__ counts,
+                                                             const int* __restrict__ indices,
+                                                             int* __restrict__ report) {
+  const int row = int(blockIdx.x) * 4 + int(threadIdx.x >> 6);
+  if (row >= rows) return;
+  const int lane = threadIdx.x & 63;
+  const int c = counts[row];
+  int bad = 0;
+  if (c < 0 || c > NB) {
+    bad = kListBadCount;
+  } else {
+    const int* ind = indices + int64_t(row) * NB;
+    for (int e = lane; e < c; e += 64) {
+      const int j = ind[e];
+      if (j < 0 || j >= NB) bad |= kListBadIndex;
+      if (e > 0 && ind[e - 1] >= j) bad |= kListNotAscending;
+    }
+    bad = (__ballot(bad & kListBadCount) ? kListBadCount : 0) |
+          (__ballot(bad & kListBadIndex) ? kListBadIndex : 0) |
+          (__ballot(bad & kListNotAscending) ? kListNotAscending : 0);
+  }
+  if (bad != 0 && lane == 0) {
+    atomicAdd(report, 1);
+    atomicMin(report + 1, row);
+    atomicOr(report + 2, bad);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_validate_lists(int NB, int rows, const int* counts, const int* indices,
+                                 int* report, hipStream_t s) {
+  clear_report_kernel<<<1, 64, 0, s>>>(report);
+  if (rows > 0)
+    validate_lists_kernel<<<dim3(unsigned((rows + 3) / 4)), 256, 0, s>>>(NB, rows, counts, indices,
+                                                                         report);
+  return hipGetLastError();
 }
 
 }  // namespace spade

@@ -116,6 +116,10 @@ struct SelectSpec {
   double* scores;
 };
 hipError_t launch_select(const DevGeom& g, const SelectSpec& p, hipStream_t s);
+// Failure bits of a block-list row (the values of SPADE_LIST_* in spade.h).
+constexpr int kListBadCount = 1, kListBadIndex = 2, kListNotAscending = 4;
+hipError_t launch_validate_lists(int NB, int rows, const int* counts, const int* indices,
+                                 int* report, hipStream_t s);
 
 // SICS of every candidate blocking in one pass over the raster Q and K. A region is
 // the per-axis least common multiple of the candidates' block extents, so every

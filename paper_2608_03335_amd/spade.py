@@ -26,6 +26,7 @@ SPADE_TOPK, SPADE_TOPP = 0, 1
 SPADE_EST_MEAN, SPADE_EST_DSA, SPADE_EST_DSA2 = 0, 1, 2
 SPADE_INTRA_NONE, SPADE_INTRA_THRESHOLD, SPADE_INTRA_TOPK = 0, 1, 2
 SPADE_TASK_T2V, SPADE_TASK_I2V = 0, 1
+SPADE_LIST_BAD_COUNT, SPADE_LIST_BAD_INDEX, SPADE_LIST_NOT_ASCENDING = 1, 2, 4
 
 EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_candidate_sics", "spade_aggregation_score",
@@ -34,7 +35,7 @@ EXPORTED = ("spade_block_reorder", "spade_summarize", "spade_block_summarize",
             "spade_policy_dense", "spade_policy_split", "spade_attn_workspace_bytes",
             "spade_block_sparse_attn", "spade_sparse_attn_raster",
             "spade_sparse_attn_raster_multi", "spade_sparse_attn_raster_noalloc",
-            "spade_status_string",
+            "spade_validate_lists", "spade_status_string",
             "spade_last_error")
 MAX_HEAD_LIST = 64
 
@@ -123,6 +124,7 @@ def lib() -> ctypes.CDLL:
             "spade_sparse_attn_raster_noalloc": (i32, [G, vp, vp, vp, vp, vp, f64, vp, vp, vp]),
             "spade_sparse_attn_raster_multi": (i32, [G, i32, ctypes.POINTER(spade_head_lists), vp,
                                                      vp, vp, f64, vp, vp, vp, sz, vp]),
+            "spade_validate_lists": (i32, [G, vp, vp, vp, vp]),
             "spade_status_string": (ctypes.c_char_p, [i32]),
             "spade_last_error": (ctypes.c_char_p, []),
         }
@@ -437,8 +439,39 @@ def spade_attn_workspace_bytes(g: spade_geom) -> int:
     return int(lib().spade_attn_workspace_bytes(ctypes.byref(g)))
 
 
+def spade_validate_lists(g: spade_geom, counts, indices, report, stream=None):
+    """report: int32 [4] device tensor: failing rows, lowest failing row, OR of the
+    SPADE_LIST_* bits, 0 (see spade.h)."""
+    a = _Args()
+    D = _Dims(g)
+    _check(a.run(lib().spade_validate_lists, ctypes.byref(g),
+                 a(counts, I32, D.per_block, "counts"), a(indices, I32, D.pairs, "indices"),
+                 a(report, I32, 4, "report"), stream))
+
+
+def _debug_validate(g: spade_geom, counts, indices, stream):
+    """With SPADE_DEBUG_VALIDATE=1 in the environment, the single-geometry attention
+    calls first check their lists on the device and raise SpadeError on a malformed
+    row (this waits for the stream)."""
+    if os.environ.get("SPADE_DEBUG_VALIDATE", "0") != "1":
+        return
+    dev = counts.device if isinstance(counts, torch.Tensor) else None
+    report = torch.empty(4, dtype=I32, device=dev)
+    spade_validate_lists(g, counts, indices, report, stream)
+    if stream is None or hasattr(stream, "synchronize"):
+        (stream or torch.cuda.current_stream(dev)).synchronize()
+    else:
+        torch.cuda.synchronize(dev)
+    bad, first, bits, _ = (int(x) for x in report.cpu())
+    if bad:
+        raise SpadeError(SPADE_ERR_INVALID_ARG,
+                         f"malformed block lists: {bad} rows fail, the first is row {first}, "
+                         f"failure bits {bits:#x}")
+
+
 def spade_block_sparse_attn(g: spade_geom, qb, kb, vb, counts, indices, scale: float, ob,
                             lse=None, workspace=None, stream=None):
+    _debug_validate(g, counts, indices, stream)
     a = _Args()
     D = _Dims(g)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -451,6 +484,7 @@ def spade_block_sparse_attn(g: spade_geom, qb, kb, vb, counts, indices, scale: f
 
 def spade_sparse_attn_raster(g: spade_geom, q, k, v, counts, indices, scale: float, o, lse=None,
                              workspace=None, stream=None):
+    _debug_validate(g, counts, indices, stream)
     a = _Args()
     D = _Dims(g)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -464,6 +498,7 @@ def spade_sparse_attn_raster(g: spade_geom, q, k, v, counts, indices, scale: flo
 def spade_sparse_attn_raster_noalloc(g: spade_geom, q, k, v, counts, indices, scale: float, o,
                                      lse=None, stream=None):
     """spade_sparse_attn_raster with the library's own per-GPU scratch (no workspace)."""
+    _debug_validate(g, counts, indices, stream)
     a = _Args()
     D = _Dims(g)
     _check(a.run(lib().spade_sparse_attn_raster_noalloc, ctypes.byref(g),

@@ -380,3 +380,17 @@ def test_multi_scheme_attention_errors():
     assert ws_call(NULL, need) == S.SPADE_ERR_WORKSPACE
     assert ws_call(FAKE, need - 1) == S.SPADE_ERR_WORKSPACE
     assert ws_call(MISALIGNED, need) == S.SPADE_ERR_WORKSPACE
+
+
+def test_validate_lists_errors():
+    fn = S.lib().spade_validate_lists
+    g = _g()
+    assert fn(ctypes.byref(g), FAKE, FAKE, NULL, None) == S.SPADE_ERR_INVALID_ARG   # null report
+    assert fn(ctypes.byref(g), NULL, FAKE, FAKE, None) == S.SPADE_ERR_INVALID_ARG   # null counts
+    assert fn(ctypes.byref(g), FAKE, NULL, FAKE, None) == S.SPADE_ERR_INVALID_ARG   # null indices
+    assert fn(ctypes.byref(_g(d=96)), FAKE, FAKE, FAKE, None) == S.SPADE_ERR_UNSUPPORTED
+    assert fn(ctypes.byref(_g(bt=0)), FAKE, FAKE, FAKE, None) == S.SPADE_ERR_INVALID_ARG
+    # one-token blocks, d = 64: 65535 * 33792 rows > 2^31 - 1, tensors still within limits
+    big = _g(B=1, H=65535, d=64, T=32, Hs=32, Ws=33, bt=1, bh=1, bw=1)
+    st, msg = _status(fn, ctypes.byref(big), FAKE, FAKE, FAKE, None)
+    assert st == S.SPADE_ERR_UNSUPPORTED and "rows" in msg
