@@ -411,6 +411,8 @@ __global__ void __launch_bounds__(kThreads) choose_scheme_kernel(const double* _
 // unit rows in fp64, and parks each cell's sum in LDS. Phase 2: each candidate block
 // of the region is the sum of its cells in (t, y, x) cell order; its SICS is that
 // sum's squared norm. Both orders are fixed, so the result is deterministic.
+// The plan's tables are copied to LDS first: indexed per lane group, reads from the
+// kernel arguments would be vector-memory round trips on the critical path.
 constexpr int kCandThreads = 512;
 constexpr int kCandBatch = 8;  // token rows in flight per lane group
 
@@ -420,8 +422,14 @@ __global__ void __launch_bounds__(kCandThreads)
                           const uint4* __restrict__ k) {
   constexpr int V = D / 8;
   constexpr int NG = kCandThreads / V;  // lane groups
-  extern __shared__ double cell_sum[];  // [cells][D]
+  extern __shared__ double cell_sum[];  // [cells][8][V]: a lane's 8 columns V apart (no bank conflicts)
   __shared__ int next_cell;
+  __shared__ int s_start[3][kMaxCellsAxis + 1];
+  __shared__ unsigned short s_order[kMaxCellLds / (64 * 8)];
+  __shared__ unsigned char s_bnd[kMaxCandGeoms][3][kMaxCellsAxis + 1];
+  __shared__ int s_ext[kMaxCandGeoms][3], s_nblk[kMaxCandGeoms][3];
+  __shared__ int s_nb[kMaxCandGeoms], s_b0[kMaxCandGeoms][3];  // blocks per region, first block
+  __shared__ double* s_out[kMaxCandGeoms];
   const int vec = threadIdx.x % V, grp = threadIdx.x / V;
   const int reg = blockIdx.x;
   const int rx = reg % pl.R[2], ry = (reg / pl.R[2]) % pl.R[1], rt = reg / (pl.R[2] * pl.R[1]);
@@ -430,6 +438,28 @@ __global__ void __launch_bounds__(kCandThreads)
   const int64_t bh = blockIdx.y;
   const uint4* src = (blockIdx.z ? k : q) + bh * g.N * V;
   const int ncells = pl.ncell[0] * pl.ncell[1] * pl.ncell[2];
+
+  for (int e = threadIdx.x; e < 3 * (kMaxCellsAxis + 1); e += kCandThreads)
+    s_start[e / (kMaxCellsAxis + 1)][e % (kMaxCellsAxis + 1)] =
+        pl.start[e / (kMaxCellsAxis + 1)][e % (kMaxCellsAxis + 1)];
+  for (int e = threadIdx.x; e < ncells; e += kCandThreads) s_order[e] = pl.order[e];
+  for (int e = threadIdx.x; e < pl.C * 3 * (kMaxCellsAxis + 1); e += kCandThreads) {
+    const int ci = e / (3 * (kMaxCellsAxis + 1)), r = e % (3 * (kMaxCellsAxis + 1));
+    s_bnd[ci][r / (kMaxCellsAxis + 1)][r % (kMaxCellsAxis + 1)] =
+        pl.bnd[ci][r / (kMaxCellsAxis + 1)][r % (kMaxCellsAxis + 1)];
+  }
+  if (threadIdx.x < pl.C) {
+    const int ci = threadIdx.x;
+    int nb = 1;
+    for (int a = 0; a < 3; ++a) {
+      s_ext[ci][a] = pl.ext[ci][a];
+      s_nblk[ci][a] = pl.nblk[ci][a];
+      s_b0[ci][a] = o[a] / pl.ext[ci][a];
+      nb *= pl.L[a] / pl.ext[ci][a];
+    }
+    s_nb[ci] = nb;
+    s_out[ci] = blockIdx.z ? pl.sics_k[ci] : pl.sics_q[ci];
+  }
 
   // phase 1: cell sums. Groups take cells from a shared counter, largest first, so
   // the groups finish together; a cell is always summed by one group in raster
@@ -442,14 +472,14 @@ __global__ void __launch_bounds__(kCandThreads)
     if (vec == 0) w = atomicAdd(&next_cell, 1);
     w = __shfl(w, leader, 64);
     if (w >= ncells) break;
-    const int c = pl.order[w];
+    const int c = s_order[w];
     const int cx = c % pl.ncell[2], cy = (c / pl.ncell[2]) % pl.ncell[1];
     const int ct = c / (pl.ncell[2] * pl.ncell[1]);
-    const int lo[3] = {o[0] + pl.start[0][ct], o[1] + pl.start[1][cy], o[2] + pl.start[2][cx]};
+    const int lo[3] = {o[0] + s_start[0][ct], o[1] + s_start[1][cy], o[2] + s_start[2][cx]};
     int ex[3];
-    ex[0] = max(0, min(o[0] + pl.start[0][ct + 1], G3[0]) - lo[0]);
-    ex[1] = max(0, min(o[1] + pl.start[1][cy + 1], G3[1]) - lo[1]);
-    ex[2] = max(0, min(o[2] + pl.start[2][cx + 1], G3[2]) - lo[2]);
+    ex[0] = max(0, min(o[0] + s_start[0][ct + 1], G3[0]) - lo[0]);
+    ex[1] = max(0, min(o[1] + s_start[1][cy + 1], G3[1]) - lo[1]);
+    ex[2] = max(0, min(o[2] + s_start[2][cx + 1], G3[2]) - lo[2]);
     const int n = ex[0] * ex[1] * ex[2];
     double uacc[8];
 #pragma unroll
@@ -499,42 +529,38 @@ __global__ void __launch_bounds__(kCandThreads)
       }
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) cell_sum[c * D + vec * 8 + e] = uacc[e];
+    for (int e = 0; e < 8; ++e) cell_sum[c * D + e * V + vec] = uacc[e];
   }
   __syncthreads();
 
   // phase 2: candidate blocks of this region
-  auto nb = [&](int ci) {
-    return (pl.L[0] / pl.ext[ci][0]) * (pl.L[1] / pl.ext[ci][1]) * (pl.L[2] / pl.ext[ci][2]);
-  };
   int total = 0;
-  for (int ci = 0; ci < pl.C; ++ci) total += nb(ci);
+  for (int ci = 0; ci < pl.C; ++ci) total += s_nb[ci];
   for (int w = grp; w < total; w += NG) {
     int ci = 0, j = w;
-    while (j >= nb(ci)) j -= nb(ci++);
-    const int px = pl.L[2] / pl.ext[ci][2], py = pl.L[1] / pl.ext[ci][1];
+    while (j >= s_nb[ci]) j -= s_nb[ci++];
+    const int px = pl.L[2] / s_ext[ci][2], py = pl.L[1] / s_ext[ci][1];
     const int jx = j % px, jy = (j / px) % py, jt = j / (px * py);
-    const int bt = o[0] / pl.ext[ci][0] + jt, by = o[1] / pl.ext[ci][1] + jy;
-    const int bx = o[2] / pl.ext[ci][2] + jx;
-    if (bt >= pl.nblk[ci][0] || by >= pl.nblk[ci][1] || bx >= pl.nblk[ci][2]) continue;
+    const int bt = s_b0[ci][0] + jt, by = s_b0[ci][1] + jy, bx = s_b0[ci][2] + jx;
+    if (bt >= s_nblk[ci][0] || by >= s_nblk[ci][1] || bx >= s_nblk[ci][2]) continue;
     double u[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) u[e] = 0.0;
-    for (int ct = pl.bnd[ci][0][jt]; ct < pl.bnd[ci][0][jt + 1]; ++ct)
-      for (int cy = pl.bnd[ci][1][jy]; cy < pl.bnd[ci][1][jy + 1]; ++cy)
-        for (int cx = pl.bnd[ci][2][jx]; cx < pl.bnd[ci][2][jx + 1]; ++cx) {
-          const double* cs = cell_sum + ((ct * pl.ncell[1] + cy) * pl.ncell[2] + cx) * D + vec * 8;
+    for (int ct = s_bnd[ci][0][jt]; ct < s_bnd[ci][0][jt + 1]; ++ct)
+      for (int cy = s_bnd[ci][1][jy]; cy < s_bnd[ci][1][jy + 1]; ++cy)
+        for (int cx = s_bnd[ci][2][jx]; cx < s_bnd[ci][2][jx + 1]; ++cx) {
+          const double* cs = cell_sum + ((ct * pl.ncell[1] + cy) * pl.ncell[2] + cx) * D + vec;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) u[e] += cs[e];
+          for (int e = 0; e < 8; ++e) u[e] += cs[e * V];
         }
     double ss = 0.0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) ss += u[e] * u[e];
     ss = row_group_sum<V>(ss);
     if (vec == 0) {
-      const int NBc = pl.nblk[ci][0] * pl.nblk[ci][1] * pl.nblk[ci][2];
-      const int64_t blk = (int64_t(bt) * pl.nblk[ci][1] + by) * pl.nblk[ci][2] + bx;
-      (blockIdx.z ? pl.sics_k[ci] : pl.sics_q[ci])[bh * NBc + blk] = ss;
+      const int NBc = s_nblk[ci][0] * s_nblk[ci][1] * s_nblk[ci][2];
+      const int64_t blk = (int64_t(bt) * s_nblk[ci][1] + by) * s_nblk[ci][2] + bx;
+      s_out[ci][bh * NBc + blk] = ss;
     }
   }
 }
