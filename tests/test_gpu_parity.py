@@ -278,6 +278,67 @@ def test_attention_is_deterministic():
     assert torch.equal(first.view(torch.int16), p.O.view(torch.int16))
 
 
+@pytest.mark.parametrize("raster", [True, False], ids=["raster", "blocked"])
+def test_attention_at_the_block_count_limit(raster):
+    """NB = 16384, the attention call's limit (the kept list of a work item is staged in
+    64 KB of LDS): one row keeps every block, one 8000, one a single block, one none;
+    the rest 8 random blocks. Sampled rows against the oracle on the same lists."""
+    cfg = P.small_cfg(16, 64, 64, 1, 2, 2, d=64, H=1, B=1)  # blocks of 4 tokens
+    og, g = P.geometry(cfg), _geom(cfg)
+    NB = g.NB
+    assert NB == 16384
+    _say("attention at NB", NB, "raster" if raster else "blocked")
+    Q, K, V = P.bf16_inputs(cfg, seed=5)
+    rng = np.random.default_rng(5)
+    counts = np.full((1, 1, NB), 8, np.int32)
+    counts[0, 0, 0] = NB
+    counts[0, 0, 12345] = 8000
+    counts[0, 0, NB - 1] = 1
+    counts[0, 0, 777] = 0
+    # lists built on the device (1 GiB); entries past a row's count are not read.
+    # 8 strictly ascending blocks per row: cumulative gaps in [1, NB/8)
+    i = torch.zeros((1, 1, NB, NB), dtype=torch.int32, device=DEV)
+    eight = np.cumsum(rng.integers(1, NB // 8, size=(NB, 8)), axis=1) - 1
+    i[0, 0, :, :8] = torch.from_numpy(eight.astype(np.int32)).to(DEV)
+    i[0, 0, 0] = torch.arange(NB, dtype=torch.int32, device=DEV)
+    i[0, 0, 12345, :8000] = torch.from_numpy(
+        np.sort(rng.choice(NB, 8000, replace=False)).astype(np.int32)).to(DEV)
+    i[0, 0, NB - 1, 0] = NB - 1
+    c = torch.from_numpy(counts).to(DEV)
+    scale = P.scale_of(cfg["d"])
+    ws = torch.empty(max(S.spade_attn_workspace_bytes(g), 1), dtype=torch.uint8, device=DEV)
+    lse = torch.full((1, 1, g.N if raster else NB * g.BS), float("nan"), dtype=torch.float32,
+                     device=DEV)
+    if raster:
+        o = torch.full_like(Q, float("nan"))
+        S.spade_sparse_attn_raster(g, Q, K, V, c, i, scale, o, lse, workspace=ws)
+    else:
+        blk = [torch.empty((1, 1, NB * g.BS, cfg["d"]), dtype=torch.bfloat16, device=DEV)
+               for _ in range(3)]
+        for x, xb in zip((Q, K, V), blk):
+            S.spade_block_reorder(g, x, xb)
+        ob = torch.full_like(blk[0], float("nan"))
+        S.spade_block_sparse_attn(g, *blk, c, i, scale, ob, lse, workspace=ws)
+        o = torch.empty_like(Q)
+        S.spade_block_reorder(g, ob, o, inverse=True)
+    torch.cuda.synchronize()
+    got = P.to_np64(o)
+    got_lse = lse.cpu().numpy().astype(np.float64)
+    if not raster:
+        got_lse = got_lse[:, :, O.token_position(og)]
+    toks = P.row_tokens(og, 777)
+    assert np.all(got[0, 0, toks] == 0) and np.all(np.isneginf(got_lse[0, 0, toks]))
+    rows = [(0, 0, r) for r in (0, 12345, NB - 1, 1, 4096, 9999, 16000)]
+    idx = np.zeros((1, 1, NB, NB), np.int32)  # host copy of the compared rows only
+    for (_, _, r) in rows:
+        idx[0, 0, r] = i[0, 0, r].cpu().numpy()
+    ref_o, ref_l = P.oracle_attention_on_lists(P.to_np64(Q), P.to_np64(K), P.to_np64(V), og,
+                                               counts, idx, scale, rows=rows)
+    worst = P.compare_rows_raster(got, got_lse, ref_o, ref_l, og, rows)
+    _say(f"  max-abs {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
+
+
 # ---------------- full attention-layer shapes, bench launch configuration ----------------
 @pytest.mark.parametrize("name,n_rows", [("wan13b", 24), ("hunyuan", 24)])
 def test_full_shape_pipeline(name, n_rows):
