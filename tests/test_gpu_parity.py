@@ -339,6 +339,44 @@ def test_attention_at_the_block_count_limit(raster):
     assert worst <= P.ATTN_MAX_ABS
 
 
+def test_attention_beyond_the_ranked_pairs():
+    """4200 (batch, head) pairs, beyond the 4096 the head ranking covers: the launch runs
+    in grid order with no schedule scratch. Sampled rows of both batch elements against
+    the oracle on the same lists; the allocation-free call must give the same bits."""
+    T, Hs, Ws, bt, bh, bw = 2, 4, 4, 2, 4, 2  # NB = 2 blocks of 16 tokens
+    cfg = P.small_cfg(T, Hs, Ws, bt, bh, bw, d=64, H=2100, B=2)
+    og, g = P.geometry(cfg), _geom(cfg)
+    _say("attention beyond the ranked pairs:", g.B * g.H, "pairs")
+    assert g.B * g.H > 4096 and S.spade_attn_workspace_bytes(g) == 0
+    Q, K, V = P.bf16_inputs(cfg, seed=7)
+    rng = np.random.default_rng(7)
+    NB = g.NB
+    counts = rng.integers(1, NB + 1, size=(g.B, g.H, NB)).astype(np.int32)
+    idx = np.zeros((g.B, g.H, NB, NB), np.int32)
+    for r in np.ndindex(g.B, g.H, NB):
+        idx[r][: counts[r]] = np.sort(rng.choice(NB, counts[r], replace=False))
+    c, i = torch.from_numpy(counts).to(DEV), torch.from_numpy(idx).to(DEV)
+    scale = P.scale_of(cfg["d"])
+    o = torch.full_like(Q, float("nan"))
+    lse = torch.full((g.B, g.H, g.N), float("nan"), dtype=torch.float32, device=DEV)
+    S.spade_sparse_attn_raster(g, Q, K, V, c, i, scale, o, lse)
+    o2 = torch.full_like(Q, float("nan"))
+    S.spade_sparse_attn_raster_noalloc(g, Q, K, V, c, i, scale, o2)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
+    got, got_lse = P.to_np64(o), lse.cpu().numpy().astype(np.float64)
+    assert np.all(np.isfinite(got)) and np.all(np.isfinite(got_lse))
+    rows = [(b, h, j) for b in range(g.B) for h in (0, 1, 1024, 2047, 2048, 2099) for j in range(NB)]
+    rows += [(int(b), int(h), int(j)) for b, h, j in zip(rng.integers(0, g.B, 40),
+                                                         rng.integers(0, g.H, 40),
+                                                         rng.integers(0, NB, 40))]
+    ref_o, ref_l = P.oracle_attention_on_lists(P.to_np64(Q), P.to_np64(K), P.to_np64(V), og,
+                                               counts, idx, scale, rows=rows)
+    worst = P.compare_rows_raster(got, got_lse, ref_o, ref_l, og, rows)
+    _say(f"  max-abs {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
+
+
 # ---------------- full attention-layer shapes, bench launch configuration ----------------
 @pytest.mark.parametrize("name,n_rows", [("wan13b", 24), ("hunyuan", 24)])
 def test_full_shape_pipeline(name, n_rows):
