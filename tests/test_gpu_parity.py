@@ -139,6 +139,29 @@ def test_selection(name, rule):
     P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(), mode, tau)
 
 
+@pytest.mark.parametrize("rule", [("topk", 3, None), ("topp", None, 0.9)], ids=["topk-3", "topp-0.9"])
+@pytest.mark.parametrize("name", ["ragged_d128", "w4_ragged", "many_blocks"])
+def test_selection_two_batch_elements(name, rule):
+    """B = 2: scores and lists of both batch elements against the oracle (the
+    workgroups' (batch, head, row group) items are dealt across the batch)."""
+    mode, k, tau = rule
+    cfg = dict(_case(name), B=2)
+    _say("selection B=2", name, rule)
+    p = _path(cfg, mode=mode, topk=k, tau=tau)
+    Q, K, V = P.bf16_inputs(cfg, seed=11)
+    p.reorder_in(Q, K, V)
+    p.summarize()
+    p.counts.fill_(-1)
+    scores = torch.full((2, cfg["H"], p.g.NB, p.g.NB), float("nan"), dtype=torch.float64,
+                        device=DEV)
+    S.spade_estimate_select(p.g, p.qbar, p.kbar, p.mode, p.topk, p.tau, p.scale, p.counts,
+                            p.indices, scores)
+    torch.cuda.synchronize()
+    s, c, i = _oracle_selection(cfg, Q, K, mode, k, tau)
+    np.testing.assert_allclose(scores.cpu().numpy(), s, rtol=1e-12, atol=1e-12)
+    P.compare_selection(s, c, i, p.counts.cpu().numpy(), p.indices.cpu().numpy(), mode, tau)
+
+
 def _attention_vs_oracle(cfg, p, Q, K, V, counts, indices, rows=None):
     og = P.geometry(cfg)
     ci = torch.from_numpy(counts).to(DEV)
