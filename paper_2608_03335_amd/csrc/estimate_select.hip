@@ -40,6 +40,8 @@ namespace spade {
 namespace {
 
 constexpr int kRows = 12;
+template <int D>
+constexpr int kQsStride = D + 2;  // doubles per staged query row
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 // Register slots per lane of a row's keys (element e = 64 s + lane): SM slots
@@ -273,12 +275,13 @@ __device__ void intra_topk_marks(const DevGeom& g, const double* sics, int k, in
   }
 }
 
-// Rows of up to 512 blocks (SM <= 8) fit in 128 VGPRs outside the DSA estimator:
-// up to four waves per SIMD; the LDS (12 score rows + histograms) allows three
-// workgroups per CU.
+// Rows of up to 512 blocks (SM <= 8) fit in 128 VGPRs with the DSA2 estimator (up to
+// four waves per SIMD) and in 168 with the mean estimator, whose score phase holds two
+// key tiles (three waves per SIMD); the LDS (12 score rows + histograms) allows three
+// workgroups per CU either way.
 template <int D, int EST, int SM>
 __global__ void __launch_bounds__(kThreads)
-    __attribute__((amdgpu_waves_per_eu(SM <= 8 && EST != kEstDsa ? 4 : 1)))
+    __attribute__((amdgpu_waves_per_eu(SM <= 8 && EST != kEstDsa ? (EST == kEstMean ? 3 : 4) : 1)))
     select_kernel(DevGeom g, SelectSpec p) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int NB = g.NB;
@@ -311,6 +314,56 @@ __global__ void __launch_bounds__(kThreads)
   if (EST != kEstDsa2) {
     // MFMA step (kq, h) contracts d = 8*kq + 2*g4 + h, g4 = lane/16 the k-slot.
     // DSA: A = q~ = (qmax + qmin)/2 against B = k_c, then |q~| against k_r.
+    if (EST == kEstMean) {
+      // The item's query summaries (16 rows: the tile's rows past the item zero) are
+      // staged in LDS, in the area the selection phase later uses for its histograms:
+      // the A operand is read from there, which leaves the registers to hold two key
+      // tiles, so the next tile's loads are in flight while this one is contracted.
+      // Rows padded to D + 2 doubles: the 16 rows a quarter wave reads hit distinct banks.
+      double* qs = reinterpret_cast<double*>(hist_w);  // [16][kQsStride]
+      for (int e = threadIdx.x; e < 16 * D; e += kThreads) {
+        const int r = e / D, row = i0 + r;
+        qs[r * kQsStride<D> + e % D] = (r < kRows && row < NB) ? q0[int64_t(row) * D + e % D] : 0.0;
+      }
+      __syncthreads();
+      auto load_k = [&](double2 (&kv)[KQ], int jt) {
+        const int col = jt * 16 + r16;
+        const double2* pk = reinterpret_cast<const double2*>(k0 + int64_t(min(col, NB - 1)) * D) + g4;
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) kv[kq] = pk[4 * kq];
+      };
+      auto tile = [&](const double2 (&kv)[KQ], int jt) {
+        const int col = jt * 16 + r16;
+        const double* qrow = qs + r16 * kQsStride<D> + 2 * g4;
+        f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int kq = 0; kq < KQ; ++kq) {
+          const double2 a = *reinterpret_cast<const double2*>(qrow + 8 * kq);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a.x, kv[kq].x, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a.y, kv[kq].y, acc, 0, 0, 0);
+        }
+        if (col < NB) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {  // acc[r] = S[4r + g4][r16]
+            const int rr = 4 * r + g4;  // tile rows past kRows belong to the next item
+            const double sv = acc[r] * p.scale + 0.0;  // + 0.0 folds -0 into +0
+            if (rr < kRows) sc[rr * NB + col] = sv;
+            if (p.scores && rr < kRows && i0 + rr < NB) p.scores[(bh * NB + i0 + rr) * NB + col] = sv;
+          }
+        }
+      };
+      double2 kA[KQ], kB[KQ];
+      int jt = wave;
+      if (jt < ntiles) load_k(kA, jt);
+      for (; jt < ntiles; jt += 2 * kWaves) {
+        const int jt1 = jt + kWaves;
+        if (jt1 < ntiles) load_k(kB, jt1);
+        tile(kA, jt);
+        if (jt1 >= ntiles) break;
+        if (jt1 + kWaves < ntiles) load_k(kA, jt1 + kWaves);
+        tile(kB, jt1);
+      }
+    } else {
     double qa[2 * KQ];
     {
       const int row = i0 + r16;
@@ -365,6 +418,7 @@ __global__ void __launch_bounds__(kThreads)
         }
       }
     }
+    }
   } else {
     // DSA2 on the VALU: lane (r16, g4) scores column jt*16 + r16 against rows
     // 4r + g4, summing channels in order.
@@ -400,6 +454,7 @@ __global__ void __launch_bounds__(kThreads)
     }
   }
 
+  __syncthreads();  // staged query rows dead: their area becomes the histograms
   // ---------------- composition inputs ----------------
   const bool window = p.wt >= 0;
   const bool extras = p.intra != kIntraNone || window || p.sink > 0;
@@ -513,11 +568,17 @@ __global__ void __launch_bounds__(kThreads)
 
 template <int D, int EST, int SM>
 hipError_t launch_des(const DevGeom& g, const SelectSpec& p, hipStream_t s) {
-  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + kWaves * 256 * 8 +
-                     size_t(g.NB) * (4 + 1) + kRows;
+  // after the score rows: the histograms and marks of the selection phase, sharing
+  // their area with the staged query rows of the score phase
+  auto tail = [](int NB) {
+    const size_t sel = size_t(kWaves) * 256 * 8 + size_t(NB) * (4 + 1) + kRows;
+    const size_t qst = EST == kEstMean ? size_t(16) * kQsStride<D> * sizeof(double) : 0;
+    return sel > qst ? sel : qst;
+  };
+  const size_t lds = size_t(kRows) * g.NB * sizeof(double) + tail(g.NB);
   const hipError_t e = ensure_dynamic_lds(
       reinterpret_cast<const void*>(&select_kernel<D, EST, SM>),
-      int(kRows * kMaxSelectNB * sizeof(double) + kWaves * 256 * 8 + kMaxSelectNB * 5 + kRows));
+      int(kRows * kMaxSelectNB * sizeof(double) + tail(kMaxSelectNB)));
   if (e != hipSuccess) return e;
   const int64_t items = int64_t(g.B) * g.H * ((g.NB + kRows - 1) / kRows);
   const dim3 grid(unsigned((items + 7) / 8 * 8));  // see the XCD mapping in the kernel
