@@ -51,7 +51,8 @@
  *   - Limits: d in {64, 128}; BS <= 256; NB <= 1024 for the selection call and
  *     NB <= 16384 for the attention call.
  *     B, H, T, Hs or Ws equal to 0 is an empty problem: the call returns
- *     SPADE_OK without launching anything (pointers are then not read).
+ *     SPADE_OK without launching anything (pointers are then not read), except
+ *     spade_validate_lists, which still clears its report.
  */
 #ifndef SPADE_H
 #define SPADE_H
