@@ -40,6 +40,11 @@ def _case(name):
         # paired-wave kernel (5 row tiles): ragged on every axis; a 5th tile of 8 rows
         "pp_ragged_d64": dict(T=7, Hs=11, Ws=19, bt=4, bh=5, bw=8, d=64, H=2),  # BS 160
         "pp_bs136": dict(T=5, Hs=19, Ws=16, bt=1, bh=17, bw=8, d=128, H=2),     # BS 136
+        # the paired kernel's smallest block: a 5th tile of one row, a last chunk of one key
+        "pp_bs129": dict(T=2, Hs=7, Ws=50, bt=1, bh=3, bw=43, d=128, H=2),      # BS 129
+        # single-member workgroups of 3 and 7 compute waves (with a loader), ragged
+        "w3_ragged": dict(T=5, Hs=11, Ws=20, bt=2, bh=4, bw=9, d=128, H=2),     # BS 72
+        "w7_ragged_d64": dict(T=3, Hs=21, Ws=23, bt=2, bh=10, bw=10, d=64, H=2),  # BS 200
         # NB 1000 (ragged), near the selection limit: 125 query blocks per XCD share,
         # so the heaviest-first ranking of work items runs over two windows of 64 rows
         "many_blocks": dict(T=4, Hs=19, Ws=49, bt=1, bh=2, bw=2, d=64, H=2),   # BS 4
@@ -50,7 +55,8 @@ def _case(name):
 
 
 SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block",
-         "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136", "many_blocks"]
+         "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136", "pp_bs129",
+         "w3_ragged", "w7_ragged_d64", "many_blocks"]
 
 
 def _say(*a):

@@ -48,7 +48,8 @@ def test_raster_equals_blocked_then_restore(name):
     assert torch.equal(lse, p.lse[:, :, pos])
 
 
-@pytest.mark.parametrize("name", ["tiny", "ragged_d64", "bs144_tail", "one_block", "w4_ragged", "w6_ragged"])
+@pytest.mark.parametrize("name", ["tiny", "ragged_d64", "bs144_tail", "one_block", "w4_ragged", "w6_ragged",
+                                  "pp_bs129", "w3_ragged"])
 def test_virtual_path_matches_oracle(name):
     """The whole virtual path: selection against the oracle's (cut exemptions
     allowed), and the attention output, NaN-poisoned before the call, against the
