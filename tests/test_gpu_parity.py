@@ -368,6 +368,68 @@ def test_attention_at_the_block_count_limit(raster):
     assert worst <= P.ATTN_MAX_ABS
 
 
+@pytest.mark.parametrize("raster", [True, False], ids=["raster", "blocked"])
+def test_attention_five_tiles_beyond_the_paired_list_space(raster):
+    """Blocks of 129..160 slots go to the paired kernel only while its LDS holds the
+    kept list beside the 8-chunk ring (d = 128: NB <= 7928); beyond, the 5-wave
+    single-member kernel takes them. NB = 8000 of 136-slot blocks: one row keeps every
+    block, one 5000, one a single block, one none, the rest 6 random blocks; sampled
+    rows against the oracle on the same lists."""
+    cfg = P.small_cfg(16, 425, 160, 1, 17, 8, d=128, H=1, B=1)  # 16 x 25 x 20 blocks
+    og, g = P.geometry(cfg), _geom(cfg)
+    NB = g.NB
+    assert NB == 8000 and g.BS == 136
+    _say("attention, 5 row tiles at NB", NB, "raster" if raster else "blocked")
+    Q, K, V = P.bf16_inputs(cfg, seed=6)
+    rng = np.random.default_rng(6)
+    counts = np.full((1, 1, NB), 6, np.int32)
+    counts[0, 0, 0] = NB
+    counts[0, 0, 4321] = 5000
+    counts[0, 0, NB - 1] = 1
+    counts[0, 0, 555] = 0
+    i = torch.zeros((1, 1, NB, NB), dtype=torch.int32, device=DEV)
+    six = np.cumsum(rng.integers(1, NB // 6, size=(NB, 6)), axis=1) - 1
+    i[0, 0, :, :6] = torch.from_numpy(six.astype(np.int32)).to(DEV)
+    i[0, 0, 0] = torch.arange(NB, dtype=torch.int32, device=DEV)
+    i[0, 0, 4321, :5000] = torch.from_numpy(
+        np.sort(rng.choice(NB, 5000, replace=False)).astype(np.int32)).to(DEV)
+    i[0, 0, NB - 1, 0] = 17
+    c = torch.from_numpy(counts).to(DEV)
+    scale = P.scale_of(cfg["d"])
+    ws = torch.empty(max(S.spade_attn_workspace_bytes(g), 1), dtype=torch.uint8, device=DEV)
+    lse = torch.full((1, 1, g.N if raster else NB * g.BS), float("nan"), dtype=torch.float32,
+                     device=DEV)
+    if raster:
+        o = torch.full_like(Q, float("nan"))
+        S.spade_sparse_attn_raster(g, Q, K, V, c, i, scale, o, lse, workspace=ws)
+    else:
+        blk = [torch.empty((1, 1, NB * g.BS, cfg["d"]), dtype=torch.bfloat16, device=DEV)
+               for _ in range(3)]
+        for x, xb in zip((Q, K, V), blk):
+            S.spade_block_reorder(g, x, xb)
+        ob = torch.full_like(blk[0], float("nan"))
+        S.spade_block_sparse_attn(g, *blk, c, i, scale, ob, lse, workspace=ws)
+        o = torch.empty_like(Q)
+        S.spade_block_reorder(g, ob, o, inverse=True)
+    torch.cuda.synchronize()
+    got = P.to_np64(o)
+    got_lse = lse.cpu().numpy().astype(np.float64)
+    if not raster:
+        got_lse = got_lse[:, :, O.token_position(og)]
+    assert np.all(np.isfinite(got)), "every output row is written"
+    toks = P.row_tokens(og, 555)
+    assert np.all(got[0, 0, toks] == 0) and np.all(np.isneginf(got_lse[0, 0, toks]))
+    rows = [(0, 0, r) for r in (0, 4321, NB - 1, 1, 2500, 7999 - 20)]
+    idx = np.zeros((1, 1, NB, NB), np.int32)  # host copy of the compared rows only
+    for (_, _, r) in rows:
+        idx[0, 0, r] = i[0, 0, r].cpu().numpy()
+    ref_o, ref_l = P.oracle_attention_on_lists(P.to_np64(Q), P.to_np64(K), P.to_np64(V), og,
+                                               counts, idx, scale, rows=rows)
+    worst = P.compare_rows_raster(got, got_lse, ref_o, ref_l, og, rows)
+    _say(f"  max-abs {worst:.3e}")
+    assert worst <= P.ATTN_MAX_ABS
+
+
 def test_attention_beyond_the_ranked_pairs():
     """4200 (batch, head) pairs, beyond the 4096 the head ranking covers: the launch runs
     in grid order with no schedule scratch. Sampled rows of both batch elements against
