@@ -160,6 +160,14 @@ def test_compose_select_matches_oracle(name, which):
     _say(f"  exempt rows {n_ex}")
 
 
+@pytest.mark.parametrize("which", ["mean_plain", "dsa_topk_intra_window_sink", "dsa2_topp_intra_topk"])
+@pytest.mark.parametrize("name", ["nb384", "many_blocks"])
+def test_compose_select_wide_rows(name, which):
+    """Rows of 257..512 and 513..1024 blocks (NB 384 and 1000): the selection kernel's
+    wider register layouts, for every estimator, the intra filters and the window."""
+    test_compose_select_matches_oracle(name, which)
+
+
 @pytest.mark.parametrize("name", ["tiny", "ragged_d128", "w4_ragged"])
 def test_compose_mean_plain_equals_estimate_select(name):
     cfg = _case(name)

@@ -48,6 +48,8 @@ def _case(name):
         # NB 1000 (ragged), near the selection limit: 125 query blocks per XCD share,
         # so the heaviest-first ranking of work items runs over two windows of 64 rows
         "many_blocks": dict(T=4, Hs=19, Ws=49, bt=1, bh=2, bw=2, d=64, H=2),   # BS 4
+        # NB 384: rows of the selection kernel's middle register width (257..512 blocks)
+        "nb384": dict(T=4, Hs=24, Ws=32, bt=1, bh=2, bw=4, d=128, H=2),       # BS 8
     }
     kw = dict(table[name])
     return P.small_cfg(kw.pop("T"), kw.pop("Hs"), kw.pop("Ws"), kw.pop("bt"), kw.pop("bh"),
