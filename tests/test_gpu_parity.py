@@ -45,6 +45,9 @@ def _case(name):
         # single-member workgroups of 3 and 7 compute waves (with a loader), ragged
         "w3_ragged": dict(T=5, Hs=11, Ws=20, bt=2, bh=4, bw=9, d=128, H=2),     # BS 72
         "w7_ragged_d64": dict(T=3, Hs=21, Ws=23, bt=2, bh=10, bw=10, d=64, H=2),  # BS 200
+        # d = 64 for the 6- and 8-wave workgroups
+        "w6_ragged_d64": dict(T=7, Hs=13, Ws=23, bt=3, bh=6, bw=10, d=64, H=2),  # BS 180
+        "bs256_d64": dict(T=8, Hs=16, Ws=12, bt=4, bh=8, bw=8, d=64, H=1),       # BS 256
         # NB 1000 (ragged), near the selection limit: 125 query blocks per XCD share,
         # so the heaviest-first ranking of work items runs over two windows of 64 rows
         "many_blocks": dict(T=4, Hs=19, Ws=49, bt=1, bh=2, bw=2, d=64, H=2),   # BS 4
@@ -58,7 +61,7 @@ def _case(name):
 
 SMALL = ["tiny", "ragged_d64", "ragged_d128", "bs144_tail", "bs256_max", "one_token", "one_block",
          "w4_ragged", "w4_ragged_d64", "w6_ragged", "pp_ragged_d64", "pp_bs136", "pp_bs129",
-         "w3_ragged", "w7_ragged_d64", "many_blocks"]
+         "w3_ragged", "w7_ragged_d64", "w6_ragged_d64", "bs256_d64", "many_blocks"]
 
 
 def _say(*a):
