@@ -1,0 +1,91 @@
+"""Calls that overlap: the library keeps no state between calls beyond the
+allocation-free call's scratch, so two paths with their own buffers and workspaces,
+issued on two streams without any ordering between them, and calls from several
+host threads at once, must each give what the same call gives alone."""
+import sys
+import threading
+
+import pytest
+import torch
+
+from paper_2608_03335_amd import spade as S
+from paper_2608_03335_amd.pipeline import SpadePath
+
+from . import _parity as P
+from .test_gpu_parity import _case
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _path(cfg):
+    return SpadePath(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"],
+                     cfg["bh"], cfg["bw"], mode=cfg["mode"], topk=cfg.get("topk"),
+                     tau=cfg.get("tau"), device=DEV, virtual=True, with_lse=True)
+
+
+def _alone(cfg, seed):
+    Q, K, V = P.bf16_inputs(cfg, seed=seed)
+    p = _path(cfg)
+    p.run(Q, K, V)
+    torch.cuda.synchronize()
+    return (Q, K, V), (p.O.clone(), p.lse.clone(), p.counts.clone())
+
+
+def _same(p, ref):
+    o, lse, c = ref
+    return (torch.equal(p.O.view(torch.int16), o.view(torch.int16)) and torch.equal(p.lse, lse)
+            and torch.equal(p.counts, c))
+
+
+def test_two_streams_without_ordering():
+    cases = [("bs144_tail", 21), ("w4_ragged", 22)]
+    _say("two streams:", cases)
+    alone = [_alone(_case(n), s) for n, s in cases]
+    paths = [_path(_case(n)) for n, _ in cases]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]  # default priority
+    for rep in range(3):
+        for p in paths:
+            P.nan_fill(p.O, p.lse)
+        torch.cuda.synchronize()
+        for p, s, (qkv, _) in zip(paths, streams, alone):
+            with torch.cuda.stream(s):
+                p.run(*qkv, stream=s)
+        torch.cuda.synchronize()
+        for p, (_, ref) in zip(paths, alone):
+            assert _same(p, ref), f"round {rep}"
+
+
+def test_host_threads():
+    names = ["bs144_tail", "w4_ragged", "pp_ragged_d64", "ragged_d64"]
+    _say("four host threads:", names)
+    alone = [_alone(_case(n), 30 + k) for k, n in enumerate(names)]
+    errors = []
+
+    def work(k):
+        try:
+            cfg = _case(names[k])
+            p = _path(cfg)
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(5):
+                    P.nan_fill(p.O, p.lse)
+                    p.run(*alone[k][0], stream=s)
+                    s.synchronize()
+                    if not _same(p, alone[k][1]):
+                        errors.append(f"{names[k]}: differs from the call alone")
+                        return
+        except Exception as exc:  # reported below, in the main thread
+            errors.append(f"{names[k]}: {exc!r}")
+
+    threads = [threading.Thread(target=work, args=(k,)) for k in range(len(names))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
