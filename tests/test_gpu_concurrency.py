@@ -89,3 +89,38 @@ def test_host_threads():
     for t in threads:
         t.join()
     assert not errors, errors
+
+
+@pytest.mark.parametrize("name", ["bs144_tail", "w4_ragged"])
+def test_non_finite_values_stay_in_their_head(name):
+    """NaN and inf in one head's Q and K (selection and attention both read them): the
+    call completes, its block lists are well-formed, and the other head's lists and
+    outputs equal those of a clean run, bit for bit."""
+    cfg = _case(name)
+    assert cfg["H"] >= 2
+    _say("non-finite values in head 0:", name)
+    Q, K, V = P.bf16_inputs(cfg, seed=41)
+    clean = _path(cfg)
+    clean.run(Q, K, V)
+    torch.cuda.synchronize()
+    Qb, Kb = Q.clone(), K.clone()
+    Qb[:, 0, 5, :] = float("nan")
+    Kb[:, 0, 17, :] = float("inf")
+    Kb[:, 0, 40, 3] = float("nan")
+    p = _path(cfg)
+    p.run(Qb, Kb, V)
+    torch.cuda.synchronize()
+    g = S.geom(cfg["B"], cfg["H"], cfg["d"], cfg["T"], cfg["Hs"], cfg["Ws"], cfg["bt"], cfg["bh"],
+               cfg["bw"])
+    report = torch.full((4,), -9, dtype=torch.int32, device=DEV)
+    S.spade_validate_lists(g, p.counts, p.indices, report)
+    torch.cuda.synchronize()
+    assert report.cpu().tolist() == [0, 2**31 - 1, 0, 0]
+    h = slice(1, cfg["H"])
+    assert torch.equal(p.counts[:, h], clean.counts[:, h])
+    NB = g.NB
+    live = torch.arange(NB, device=DEV) < p.counts[:, h, :, None]
+    assert torch.equal(torch.where(live, p.indices[:, h], -1),
+                       torch.where(live, clean.indices[:, h], -1))
+    assert torch.equal(p.O[:, h].view(torch.int16), clean.O[:, h].view(torch.int16))
+    assert torch.equal(p.lse[:, h], clean.lse[:, h])
