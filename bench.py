@@ -157,12 +157,15 @@ def cpu_baseline(Q, K, V, cfg, budget_s: float, call_flops: float) -> dict:
 
 
 def attn_kernel_label(g) -> str:
-    """Which attention kernel the library launches for this blocking: the paired
-    kernel for blocks of 5 row tiles (129..160 slots) whose 8-chunk ring and kept
-    list fit one CU's 160 KB of LDS, the single-member kernel otherwise."""
+    """Which attention kernel the library launches for this blocking: for blocks of 5
+    row tiles (129..160 slots) the software-pipelined kernel at d = 128 when its
+    9-chunk ring and the kept list fit one CU's 160 KB of LDS, else the paired kernel
+    when its 8-chunk ring and the list fit; the single-member kernel otherwise."""
     tiles = -(-g.bt * g.bh * g.bw // 32)
-    ring = 8 * 2 * 32 * g.d * 2
-    if tiles == 5 and ring + 256 * 4 + 8 * 4 + g.NB * 4 <= 160 * 1024:
+    chunk = 2 * 32 * g.d * 2
+    if tiles == 5 and g.d == 128 and 9 * chunk + 256 * 4 + 64 + g.NB * 4 <= 160 * 1024:
+        return "spade attn_sw_kernel (software-pipelined waves, bf16 MFMA 32x32x16)"
+    if tiles == 5 and 8 * chunk + 256 * 4 + 8 * 4 + g.NB * 4 <= 160 * 1024:
         return "spade attn_pp_kernel (paired waves, bf16 MFMA 32x32x16)"
     return "spade attn_kernel (bf16 MFMA 32x32x16)"
 

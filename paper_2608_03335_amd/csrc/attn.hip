@@ -1,13 +1,17 @@
 // Flash block-sparse attention (paper Eq. (2), §3.3 optimisation (3)) on gfx950.
 //
-// One workgroup per query block (b, h, i). Two kernels share the data movement
+// One workgroup per query block (b, h, i). Three kernels share the data movement
 // and the math below:
-// - attn_kernel: wave w owns query slots 32w..32w+31; for most block sizes one
-//   more wave only issues the K/V loads.
-// - attn_pp_kernel, for blocks of 5 row tiles (129..160 slots): two waves per
-//   32-row tile split the kept walk (even / odd chunks) and alternate matrix and
-//   vector phases between barriers, so each SIMD overlaps one wave's MFMAs with
-//   the other's softmax; the pair merges by log-sum-exp.
+// - attn_sw_kernel, for blocks of 5 row tiles (129..160 slots) at d = 128: one
+//   software-pipelined wave per 32-row tile, the fifth tile split over the four
+//   DMA waves (see its comment);
+// - attn_pp_kernel, for 5-tile blocks otherwise (d = 64, or kept lists too long
+//   for the sw kernel's LDS): two waves per 32-row tile split the kept walk (even /
+//   odd chunks) and alternate matrix and vector phases between barriers, so each
+//   SIMD overlaps one wave's MFMAs with the other's softmax; the pair merges by
+//   log-sum-exp;
+// - attn_kernel for every other block size: wave w owns query slots 32w..32w+31;
+//   for most block sizes one more wave only issues the K/V loads.
 // Work items are dealt to the 8 XCDs so that all XCDs share one head at a time;
 // each XCD starts its rows of a head heaviest first (heavy_first).
 // The kept K/V blocks of row (b, h, i) are walked in ascending block order in
@@ -1045,6 +1049,463 @@ hipError_t launch_pp(const DevGeom& g, const void* qb, const void* kb, const voi
   return hipGetLastError();
 }
 
+// Software-pipelined kernel (blocks of 5 row tiles, i.e. 129..160 slots, d = 128).
+// Eight waves, two per SIMD (waves w and w + 4 share one):
+// - wave X_s (s = 0..3) owns query tile s for the whole kept walk. Its chunk loop
+//   is pipelined by one chunk: while the softmax of chunk c runs on the vector
+//   unit, the matrix unit takes P.V of chunk c-1 and S of chunk c+1 (independent
+//   of that softmax), and the K fragments of c+1 and the V^T fragments of c are
+//   read from LDS in between. One wave issues its own MFMAs and vector work
+//   interleaved; no barrier pairs it with another wave.
+// - wave Y_s issues the DMA of every fourth chunk (s, s + 4, ...) and computes
+//   tile 4 on those same chunks with its own online-softmax state; the four
+//   partial states of tile 4 merge by log-sum-exp at the end in a fixed order. So
+//   every SIMD carries 1.25 tiles of work.
+// The waves meet at one barrier per window of four chunks. A 9-slot LDS ring
+// holds the window being computed, the chunk before it and the next window in
+// flight: chunk c lives in slot c % 9; Y_s issues window v + 1 right after the
+// barrier that opens window v and waits for it before the next barrier. X's
+// iteration c reads K of c + 1 and V^T of c, so the barrier that makes window v
+// visible sits before X's iteration 4v - 1.
+constexpr int kSwRing = 9;
+constexpr int kSwWaves = 8;
+constexpr int kSwTiles = 5;
+constexpr int kSwLds = 160 * 1024;
+
+template <int D>
+struct SwLayout {
+  static constexpr int RING_BYTES = kSwRing * Tile<D>::BUF_BYTES;
+  static constexpr int REL_OFF = RING_BYTES;
+  static constexpr int KVAL_OFF = REL_OFF + kMaxBS * 4;  // real keys per ring slot
+  static constexpr int LIST_OFF = KVAL_OFF + 64;
+  static constexpr int LPC = 2 * Tile<D>::LOADS;          // DMA loads per chunk
+  static constexpr int MERGE_FLOATS = D / 32 * 16 + 2;    // per lane: O, m, l
+};
+
+template <int D, int T, bool RASTER, bool MULTI>
+__global__ void __launch_bounds__(64 * kSwWaves) __attribute__((amdgpu_waves_per_eu(2)))
+    attn_sw_kernel(DevGeom g_arg, const uint4* __restrict__ qb, const char* __restrict__ kb,
+                   const char* __restrict__ vb, const int* __restrict__ counts,
+                   const int* __restrict__ indices, float scale_log2, __bf16* __restrict__ ob,
+                   float* __restrict__ lse, const int* __restrict__ order,
+                   typename std::conditional<MULTI, MultiTable, NoTable>::type tab) {
+  static_assert(T == kSwTiles, "blocks of 5 row tiles");
+  using TL = Tile<D>;
+  using LY = SwLayout<D>;
+  constexpr int NT = 64 * kSwWaves;
+  extern __shared__ __align__(16) char smem_raw[];
+  lds_char* const lds = (lds_char*)smem_raw;
+  lds_int* const rel = (lds_int*)(smem_raw + LY::REL_OFF);
+  lds_int* const list = (lds_int*)(smem_raw + LY::LIST_OFF);
+  lds_int* const kval = (lds_int*)(smem_raw + LY::KVAL_OFF);
+
+  const Item it = work_item<MULTI>(g_arg, counts, indices, order, tab);
+  if (it.i < 0) return;
+  const DevGeom g = it.g;
+  const int64_t bh = it.bh;
+  const int i = it.i;
+  const BlockExt e_i = block_ext(g, i);
+  const int n_i = e_i.n;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool is_y = wave >= 4;
+  const int sidx = wave & 3;          // X: tile; Y: chunk residue mod 4
+  const int tile = is_y ? 4 : sidx;   // Y waves share tile 4
+  const int q0 = tile * 32;
+  const bool rows_live = tile < T && q0 < n_i;
+  const int half = lane >> 5, r32 = lane & 31;
+  const int64_t head_row = RASTER ? bh * g.N : bh * g.NB * int64_t(g.BS);
+  auto q_row = [&](int qs) -> int64_t {
+    return RASTER ? head_row + ext_token(g, e_i, qs) : head_row + int64_t(i) * g.BS + qs;
+  };
+
+  bf16x8 qf[D / 16];
+  {
+    const int qs = q0 + r32;
+    const uint4* src = qb + q_row(min(qs, n_i - 1)) * TL::NCH + half;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (rows_live && qs < n_i) v = src[2 * kk];
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
+    }
+  }
+  const int cnt = min(max(*it.cnt_src, 0), g.NB);
+  for (int e = tid; e < cnt; e += NT) list[e] = it.list_src[e];
+  if (RASTER) {
+    for (int sl = tid; sl < g.BS; sl += NT) {
+      const int q = sl / g.bw;
+      rel[sl] = ((q / g.bh) * g.Hs + q % g.bh) * g.Ws + sl % g.bw;
+    }
+  }
+  __syncthreads();
+
+  // chunks of the kept walk (every wave computes the same count)
+  int nch = 0;
+  for (int e = lane; e < cnt; e += 64) {
+    const int j = list[e];
+    if (j >= 0 && j < g.NB) nch += (block_ext(g, j).n + kChunk - 1) / kChunk;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) nch += __shfl_xor(nch, off);
+  nch = __builtin_amdgcn_readfirstlane(nch);
+  const int nbar = nch / 4 + 1;  // barriers of the chunk walk, the same for every wave
+
+  const int v_row0 = 4 * ((lane >> 4) >> 1) + ((lane & 15) >> 2);
+  const int v_piece0 = 2 * ((lane >> 4) & 1) + (((lane & 15) & 3) >> 1);
+  const int v_sub = (lane & 1) * 8;
+  const int k_off = r32 * TL::ROW_BYTES;
+  const int k_sw = swz_k<D>(r32);
+
+  f32x16 o[D / 32];
+#pragma unroll
+  for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[t][r] = 0.0f;
+  float m = -INFINITY, l = 0.0f;
+  const bf16x2 ones = {__bf16(1.0f), __bf16(1.0f)};
+  const uint32_t lds_u32 = uint32_t(reinterpret_cast<uintptr_t>(lds));
+  auto slot = [](int c) { return c % kSwRing; };
+  // the slot's base as an opaque uniform value: the compiler then adds it once per
+  // distinct lane offset instead of folding the modulo into every read address
+  auto kbuf = [&](int c) {
+    return lds + __builtin_amdgcn_readfirstlane(slot(c) * TL::BUF_BYTES);
+  };
+
+  // per-lane LDS byte offsets of the fragment reads inside a ring slot, so each read
+  // costs one add of the slot base: K fragment kk (row r32, piece 2 kk + half), and
+  // the V^T fragments of output tile t (rows 16 u + 8 h + v_row0 share row & 3, so
+  // their swizzle, and the (u, h) part goes into the instruction's offset field)
+  int kofs[D / 16], vofs[D / 32];
+#pragma unroll
+  for (int kk = 0; kk < D / 16; ++kk) kofs[kk] = k_off + (((2 * kk + half) ^ k_sw) << 4);
+#pragma unroll
+  for (int t = 0; t < D / 32; ++t)
+    vofs[t] = TL::TILE_BYTES + v_row0 * TL::ROW_BYTES +
+              ((4 * t + v_piece0) ^ swz_v<D>(v_row0)) * 16 + v_sub;
+  auto read_k = [&](int c, bf16x8 (&kf)[D / 16]) {
+    lds_char* Kt = kbuf(c);
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(lds_bf16x8*)(Kt + kofs[kk]);
+  };
+  auto read_v = [&](int c, bf16x8 (&vf)[D / 32][2]) {
+    lds_char* Vb = kbuf(c);
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t) {
+      lds_char* Vt = Vb + vofs[t];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        bf16x4 h2[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          h2[h] = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (lds_bf16x4*)(Vt + (16 * u + 8 * h) * TL::ROW_BYTES));
+        vf[t][u] = __builtin_shufflevector(h2[0], h2[1], 0, 1, 2, 3, 4, 5, 6, 7);
+      }
+    }
+  };
+  // keys past the chunk's real ones get -inf (key of s[r]: (r/4)*8 + 4*half + r%4)
+  auto mask = [&](f32x16& sv, int kv) {
+    if (kv < kChunk) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kr = (r >> 2) * 8 + 4 * half + (r & 3);
+        if (kr >= kv) sv[r] = -INFINITY;
+      }
+    }
+  };
+  // online softmax of one chunk: P (bf16) and the new running max; returns the
+  // factor that O must be scaled by (1 unless the max grew by more than 2^8)
+  auto softmax = [&](const f32x16& sv, bf16x8 (&p)[2], bool* rescale) {
+    float mx = sv[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, sv[r]);
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+    }
+    const bool rs = __any(mx > m + kRescaleLog2);
+    const float mnew = rs ? fmaxf(m, mx) : m;
+    const float alpha = __builtin_amdgcn_exp2f(m - mnew);
+    m = mnew;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(sv[r], scale_log2, -m));
+      p[r >> 3][r & 7] = __bf16(e);
+    }
+    float ls = l * alpha;
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bf16x2 pr = {p[u][2 * e], p[u][2 * e + 1]};
+        ls = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ls, false);
+      }
+    l = ls;
+    *rescale = rs;
+    return alpha;
+  };
+  auto scale_o = [&](float alpha) {
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][r] *= alpha;
+  };
+  auto pv = [&](const bf16x8 (&vf)[D / 32][2], const bf16x8 (&p)[2]) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int t = 0; t < D / 32; ++t)
+        o[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[t][u], p[u], o[t], 0, 0, 0);
+  };
+  auto s_of = [&](const bf16x8 (&kf)[D / 16]) {
+    f32x16 sv = {};
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk)
+      sv = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], sv, 0, 0, 0);
+    return sv;
+  };
+
+  if (!is_y) {
+    // ---- X: tile `tile`, every chunk, pipelined by one chunk ----
+    // One pipeline step for chunk c. In: S of c (svi), P and V^T of c - 1 (pi, vfi),
+    // and the rescale that the softmax of c - 1 asked for. Out: S of c + 1 (svo), P
+    // and V^T of c (po, vfo); the compiler folds most of the hand-over into the
+    // register allocation (a loop unrolled by two with the sets swapped spilled).
+    bool rs = false;
+    float alpha = 1.0f;
+    auto step = [&](int c, f32x16& svi, f32x16& svo, bf16x8 (&pi)[2], bf16x8 (&po)[2],
+                    bf16x8 (&vfi)[D / 32][2], bf16x8 (&vfo)[D / 32][2]) {
+      if ((c & 3) == 3) __syncthreads();  // window (c + 1) / 4 landed
+      if (rs) scale_o(alpha);  // O holds P.V up to c - 2; P of c - 1 used the new max
+      mask(svi, kval[slot(c)]);
+      // part 1: the K fragments of c + 1 (past the walk's end the slot's stale
+      // contents: that S is discarded); P.V of c - 1 on the matrix unit; on the
+      // vector unit the row sum of P of c - 1, the row max of c and the first half of
+      // its exponentials
+      lds_char* Kt = kbuf(c + 1);
+      bf16x8 kf[D / 16];
+#pragma unroll
+      for (int kk = 0; kk < D / 16; ++kk) kf[kk] = *(lds_bf16x8*)(Kt + kofs[kk]);
+      pv(vfi, pi);
+      {
+        float ls = l * alpha;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const bf16x2 pr = {pi[u][2 * e], pi[u][2 * e + 1]};
+            ls = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ls, false);
+          }
+        l = ls;
+      }
+      {
+        float mx = svi[0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, svi[r]);
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
+                                                         __float_as_uint(mx), false, false);
+        mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * scale_log2;
+        rs = __any(mx > m + kRescaleLog2);
+        const float mnew = rs ? fmaxf(m, mx) : m;
+        alpha = __builtin_amdgcn_exp2f(m - mnew);
+        m = mnew;
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+        po[0][r] = __bf16(__builtin_amdgcn_exp2f(__builtin_fmaf(svi[r], scale_log2, -m)));
+      // part 2: S of c + 1 (two accumulators: two short MFMA chains), the V^T
+      // fragments of c and the second half of the exponentials
+      read_v(c, vfo);
+      f32x16 s0 = {}, s1 = {};
+#pragma unroll
+      for (int kk = 0; kk < D / 16; kk += 2) {
+        s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], s0, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk + 1], qf[kk + 1], s1, 0, 0, 0);
+      }
+#pragma unroll
+      for (int r = 8; r < 16; ++r)
+        po[1][r - 8] = __bf16(__builtin_amdgcn_exp2f(__builtin_fmaf(svi[r], scale_log2, -m)));
+#pragma unroll
+      for (int r = 0; r < 16; ++r) svo[r] = s0[r] + s1[r];
+    };
+    __syncthreads();  // window 0 landed
+    f32x16 svA = {}, svB = {};
+    bf16x8 pA[2] = {}, pB[2] = {};              // P of the previous chunk (zero before 0)
+    bf16x8 vfA[D / 32][2] = {}, vfB[D / 32][2] = {};  // V^T of the previous chunk
+    if (rows_live && nch > 0) {
+      bf16x8 kf[D / 16];
+      read_k(0, kf);
+      svA = s_of(kf);
+    }
+    // the last chunk's P.V (after the rescale its softmax asked for)
+    auto finish = [&](bf16x8 (&vfx)[D / 32][2], bf16x8 (&px)[2]) {
+      if (rs) scale_o(alpha);
+      pv(vfx, px);
+      float ls = l * alpha;
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const bf16x2 pr = {px[u][2 * e], px[u][2 * e + 1]};
+          ls = __builtin_amdgcn_fdot2_f32_bf16(pr, ones, ls, false);
+        }
+      l = ls;
+    };
+    if (rows_live) {
+#pragma unroll 1
+      for (int c = 0; c < nch; ++c) {
+        step(c, svA, svB, pA, pB, vfA, vfB);
+        svA = svB;
+        pA[0] = pB[0];
+        pA[1] = pB[1];
+#pragma unroll
+        for (int t = 0; t < D / 32; ++t) {
+          vfA[t][0] = vfB[t][0];
+          vfA[t][1] = vfB[t][1];
+        }
+      }
+      if (nch > 0) finish(vfA, pA);
+    } else {  // no query rows here: only the barriers of the walk
+#pragma unroll 1
+      for (int c = 3; c < nch; c += 4) __syncthreads();
+    }
+  } else {
+    // ---- Y: DMA of chunks sidx, sidx + 4, ...; tile 4 on the same chunks ----
+    Cursor cur = next_chunk(g, list, nch > 0 ? cnt : 0, {-1, 0, 0, -kChunk, e_i});
+    auto advance4 = [&]() {
+#pragma unroll 1
+      for (int a = 0; a < 4; ++a) cur = next_chunk(g, list, cnt, cur);
+    };
+#pragma unroll 1
+    for (int a = 0; a < sidx; ++a) cur = next_chunk(g, list, cnt, cur);
+    int c_issue = sidx;  // next chunk this wave issues
+    auto issue = [&]() {
+      if (c_issue < nch) {
+        if (lane == 0) kval[slot(c_issue)] = min(cur.nj - cur.c0, kChunk);
+        loader_chunk<D, RASTER>(g, kb, vb, head_row, cur, rel,
+                                lds_u32 + slot(c_issue) * TL::BUF_BYTES, lane);
+        advance4();
+      }
+      c_issue += 4;
+    };
+    auto tile4 = [&](int c) {
+      if (rows_live && c < nch) {
+        bf16x8 kf[D / 16];
+        read_k(c, kf);
+        f32x16 sv = s_of(kf);
+        mask(sv, kval[slot(c)]);
+        bool rs;
+        bf16x8 pc[2];
+        const float alpha = softmax(sv, pc, &rs);
+        if (rs) scale_o(alpha);
+        bf16x8 vf[D / 32][2];
+        read_v(c, vf);
+        pv(vf, pc);
+      }
+    };
+    issue();  // window 0
+    issue();  // window 1
+    wait_chunks<LY::LPC>(sidx + 4 < nch ? 1 : 0);
+    __syncthreads();  // window 0 landed
+#pragma unroll 1
+    for (int w = 0; w + 1 < nbar; ++w) {
+      tile4(4 * w + sidx);
+      wait_chunks<LY::LPC>(0);
+      __syncthreads();  // window w + 1 landed
+      issue();          // window w + 2, into the slots of chunks 4w - 1 .. 4w + 2
+    }
+    tile4(4 * (nbar - 1) + sidx);
+  }
+
+  // tile 4: the Y waves' partial states merge in LDS (the ring is free once every
+  // wave is past its walk)
+  float* mg = reinterpret_cast<float*>(smem_raw);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (is_y && sidx > 0 && rows_live) {
+    float* dst = mg + (sidx - 1) * (LY::MERGE_FLOATS * 64);
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dst[(t * 16 + r) * 64 + lane] = o[t][r];
+    dst[(D / 32 * 16) * 64 + lane] = m;
+    dst[(D / 32 * 16 + 1) * 64 + lane] = l;
+  }
+  __syncthreads();
+  if (is_y && sidx > 0) return;
+  if (is_y && rows_live) {
+#pragma unroll 1
+    for (int k = 0; k < 3; ++k) {
+      const float* src = mg + k * (LY::MERGE_FLOATS * 64);
+      const float mB = src[(D / 32 * 16) * 64 + lane];
+      const float lB = src[(D / 32 * 16 + 1) * 64 + lane];
+      const float mm = fmaxf(m, mB);
+      const bool none = mm == -INFINITY;
+      const float aA = none ? 0.0f : __builtin_amdgcn_exp2f(m - mm);
+      const float aB = none ? 0.0f : __builtin_amdgcn_exp2f(mB - mm);
+#pragma unroll
+      for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][r] = o[t][r] * aA + src[(t * 16 + r) * 64 + lane] * aB;
+      l = l * aA + lB * aB;
+      m = mm;
+    }
+  }
+  if (tile >= T) return;
+  {
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l),
+                                                     false, false);
+    l = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  }
+  const int qs = q0 + r32;
+  if (RASTER ? qs < n_i : qs < g.BS) {
+    const bool real = qs < n_i;
+    const float inv = (real && l > 0.0f) ? 1.0f / l : 0.0f;
+    const int64_t orow = real ? q_row(qs) : head_row + int64_t(i) * g.BS + qs;
+    __bf16* dst = ob + orow * D + 4 * half;
+#pragma unroll
+    for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = __bf16(o[t][4 * rq + e] * inv);
+        *reinterpret_cast<bf16x4*>(dst + 32 * t + 8 * rq) = v;
+      }
+    if (lse && real && half == 0)
+      lse[orow] = l > 0.0f ? (m + log2f(l)) * 0.69314718055994530942f : -INFINITY;
+  }
+}
+
+template <int D, int T, bool RASTER, bool MULTI>
+hipError_t launch_sw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
+                     const int* counts, const int* indices, float scale_log2, void* ob,
+                     float* lse, hipStream_t s, const MultiTable* tab, const int* order,
+                     int nb_max) {
+  {  // the ring and the kept list exceed the 64 KB default
+    const hipError_t e = ensure_dynamic_lds(
+        reinterpret_cast<const void*>(&attn_sw_kernel<D, T, RASTER, MULTI>), kSwLds);
+    if (e != hipSuccess) return e;
+  }
+  const size_t lds = size_t(SwLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int);
+  const uint4* q4 = static_cast<const uint4*>(qb);
+  const char* k1 = static_cast<const char*>(kb);
+  const char* v1 = static_cast<const char*>(vb);
+  __bf16* o2 = static_cast<__bf16*>(ob);
+  if constexpr (MULTI) {
+    const int64_t items = int64_t(g.B) * tab->items_per_batch;
+    attn_sw_kernel<D, T, RASTER, MULTI><<<dim3(unsigned(items)), 64 * kSwWaves, lds, s>>>(
+        g, q4, k1, v1, nullptr, nullptr, scale_log2, o2, lse, order, *tab);
+  } else {
+    const int64_t items = int64_t(g.B) * g.H * ((g.NB + 7) / 8) * 8;  // see the XCD mapping
+    attn_sw_kernel<D, T, RASTER, MULTI><<<dim3(unsigned(items)), 64 * kSwWaves, lds, s>>>(
+        g, q4, k1, v1, counts, indices, scale_log2, o2, lse, order, NoTable{});
+  }
+  return hipGetLastError();
+}
+
 template <int D, int W, bool LD, bool RASTER, bool MULTI>
 hipError_t launch_dw(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                      const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
@@ -1079,12 +1540,21 @@ template <int D, bool RASTER, bool MULTI = false>
 hipError_t launch_d(const DevGeom& g, const void* qb, const void* kb, const void* vb,
                     const int* counts, const int* indices, float scale_log2, void* ob, float* lse,
                     hipStream_t s, const MultiTable* tab = nullptr, const int* order = nullptr) {
-  // the paired kernel for 5 row tiles when its ring and the kept list fit the LDS
   int nb_max = g.NB;
   if constexpr (MULTI) {
     nb_max = 0;
     for (int k = 0; k < tab->n_heads; ++k) nb_max = max(nb_max, tab->geo[tab->head[k].geom].NB);
   }
+  // 5 row tiles: the software-pipelined kernel when its ring and the kept list fit
+  // the LDS (4-tile blocks stay on attn_kernel: with one pipelined wave per tile
+  // and idle DMA waves the sw form was 15% slower there)
+  if constexpr (D == 128) {
+    if ((g.BS + 31) / 32 == kSwTiles &&
+        size_t(SwLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int) <= size_t(kSwLds))
+      return launch_sw<D, kSwTiles, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob,
+                                                   lse, s, tab, order, nb_max);
+  }
+  // otherwise the paired kernel for 5 row tiles when its ring and the kept list fit
   if ((g.BS + 31) / 32 == kPairTiles &&
       size_t(PPLayout<D>::LIST_OFF) + size_t(nb_max) * sizeof(int) <= size_t(kPairLds))
     return launch_pp<D, kPairTiles, RASTER, MULTI>(g, qb, kb, vb, counts, indices, scale_log2, ob,
