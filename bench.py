@@ -460,7 +460,8 @@ def main():
         log("cpu baseline (fp64 oracle, bounded sample)")
         cpu = cpu_baseline(Q, K, V, cfg, args.cpu_budget, kf)
 
-    traffic = traffic_record("attn.hip", args.workload)
+    # the committed counters were taken on the plain Top-P path
+    traffic = traffic_record("attn.hip", args.workload) if args.scheme == "plain" else None
     res = {
         "metric": "sparse-attn ms/call + kept-block bf16 TFLOP/s (% MFMA peak) at ~85% sparsity",
         "value": round(value, 3),
