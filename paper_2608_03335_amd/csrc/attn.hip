@@ -1275,11 +1275,16 @@ __global__ void __launch_bounds__(64 * kSwWaves) __attribute__((amdgpu_waves_per
     // register allocation (a loop unrolled by two with the sets swapped spilled).
     bool rs = false;
     float alpha = 1.0f;
+    // kv: real keys of chunk c, read one step ahead and moved to a scalar register
+    // beside the K fragments' wait, so the mask test at the top of a step waits on no
+    // LDS read (a wait there would also drain the V^T reads just issued)
+    int kv = 0;
     auto step = [&](int c, f32x16& svi, f32x16& svo, bf16x8 (&pi)[2], bf16x8 (&po)[2],
                     bf16x8 (&vfi)[D / 32][2], bf16x8 (&vfo)[D / 32][2]) {
       if ((c & 3) == 3) __syncthreads();  // window (c + 1) / 4 landed
+      const int kv_next = kval[slot(c + 1)];
       if (rs) scale_o(alpha);  // O holds P.V up to c - 2; P of c - 1 used the new max
-      mask(svi, kval[slot(c)]);
+      mask(svi, kv);
       // part 1: the K fragments of c + 1 (past the walk's end the slot's stale
       // contents: that S is discarded); P.V of c - 1 on the matrix unit; on the
       // vector unit the row sum of P of c - 1, the row max of c and the first half of
@@ -1324,6 +1329,7 @@ __global__ void __launch_bounds__(64 * kSwWaves) __attribute__((amdgpu_waves_per
         s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk], qf[kk], s0, 0, 0, 0);
         s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk + 1], qf[kk + 1], s1, 0, 0, 0);
       }
+      kv = __builtin_amdgcn_readfirstlane(kv_next);
 #pragma unroll
       for (int r = 8; r < 16; ++r)
         po[1][r - 8] = __bf16(__builtin_amdgcn_exp2f(__builtin_fmaf(svi[r], scale_log2, -m)));
@@ -1338,6 +1344,7 @@ __global__ void __launch_bounds__(64 * kSwWaves) __attribute__((amdgpu_waves_per
       bf16x8 kf[D / 16];
       read_k(0, kf);
       svA = s_of(kf);
+      kv = __builtin_amdgcn_readfirstlane(kval[slot(0)]);
     }
     // the last chunk's P.V (after the rescale its softmax asked for)
     auto finish = [&](bf16x8 (&vfx)[D / 32][2], bf16x8 (&px)[2]) {
