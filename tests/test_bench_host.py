@@ -98,3 +98,20 @@ def test_several_gpus_are_refused():
     assert r.returncode == 2
     assert "one GPU" in r.stderr
     assert r.stdout == ""
+
+
+@pytest.mark.parametrize("bt,bh,bw,d,nb,kernel", [
+    (4, 5, 8, 128, 360, "attn_sw_kernel"),     # Hunyuan's blocks: the software-pipelined kernel
+    (3, 6, 8, 128, 245, "attn_sw_kernel"),     # 144 slots, five tiles
+    (4, 5, 8, 128, 3824, "attn_sw_kernel"),    # the longest kept list its 9-chunk ring leaves room for
+    (4, 5, 8, 128, 3825, "attn_pp_kernel"),    # one more: the paired kernel's 8-chunk ring
+    (4, 5, 8, 64, 360, "attn_pp_kernel"),      # d = 64: the paired kernel
+    (4, 5, 8, 128, 7928, "attn_pp_kernel"),
+    (4, 5, 8, 128, 7929, "attn_kernel"),       # past the paired kernel's list space
+    (3, 5, 8, 128, 630, "attn_kernel"),        # 120 slots (four tiles)
+])
+def test_kernel_label_follows_the_dispatch(bt, bh, bw, d, nb, kernel):
+    """The bench names the kernel the library launches: the LDS budgets of the 5-tile
+    kernels (ring + slot table + per-slot key counts + kept list <= 160 KB)."""
+    g = SimpleNamespace(bt=bt, bh=bh, bw=bw, d=d, NB=nb)
+    assert bench.attn_kernel_label(g).split()[1] == kernel
